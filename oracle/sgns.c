@@ -1,0 +1,288 @@
+/*
+ * Oracle: the HogBatch SGNS minibatch step, a batch of snapshot steps and a
+ * sequential epoch. TEST INFRASTRUCTURE ONLY.
+ *
+ * The minibatch of Sec. 1.1 (Fig. 1 right) batches, for one target word and
+ * its N input words, the dot products of Alg. 1 into one matrix product, then
+ * writes the model updates back at the end of that product. Per input word i
+ * and output column k (column 0 = target, label 1; columns 1..K = negatives,
+ * label 0) Alg. 1 fixes: inner product of the M_in row of i with the M_out row
+ * of k, error = label - sigma(inner product), M_out row of k moves by
+ * alpha * error * (M_in row of i), M_in row of i moves by alpha * sum_k error *
+ * (M_out row of k). In the minibatch form all inner products use the rows as
+ * they were before the minibatch (the updates are written back after the
+ * product), so the step is
+ *   X = A O^T,  E = alpha (l - sigma(X)),  dA = E O,  dO = E^T A.
+ * These are alpha times the negative gradient of the skip-gram
+ * negative-sampling loss  sum_i [ -log sigma(X_i0) - sum_k log sigma(-X_ik) ].
+ */
+#include <math.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include "oracle.h"
+#include "oracle_internal.h"
+
+/* Logistic function, evaluated without overflow for either sign. */
+static double sigma(double x) {
+  if (x >= 0.0) return 1.0 / (1.0 + exp(-x));
+  double ex = exp(x);
+  return ex / (1.0 + ex);
+}
+
+/* log(sigma(x)), evaluated without overflow for either sign. */
+static double log_sigma(double x) {
+  if (x >= 0.0) return -log1p(exp(-x));
+  return x - log1p(exp(x));
+}
+
+void oracle_sgns_delta(int32_t N, int32_t K, int32_t D, const double* A,
+                       const double* O, const uint8_t* mask, double alpha,
+                       double* X, double* dA, double* dO, double* loss) {
+  const int32_t C = K + 1;
+  double* x = (double*)malloc(sizeof(double) * (size_t)(N * C + 1));
+  double* e = (double*)malloc(sizeof(double) * (size_t)(N * C + 1));
+  double total_loss = 0.0;
+  for (int32_t i = 0; i < N; ++i) {
+    for (int32_t k = 0; k < C; ++k) {
+      double inner = 0.0;
+      for (int32_t j = 0; j < D; ++j) inner += A[(size_t)i * D + j] * O[(size_t)k * D + j];
+      x[i * C + k] = inner;
+      int masked = (k > 0 && mask != NULL && mask[k - 1] != 0);
+      double label = (k == 0) ? 1.0 : 0.0;
+      e[i * C + k] = masked ? 0.0 : alpha * (label - sigma(inner));
+      if (!masked) total_loss -= (k == 0) ? log_sigma(inner) : log_sigma(-inner);
+    }
+  }
+  if (X != NULL) memcpy(X, x, sizeof(double) * (size_t)(N * C));
+  if (dA != NULL) {
+    for (int32_t i = 0; i < N; ++i)
+      for (int32_t j = 0; j < D; ++j) {
+        double acc = 0.0;
+        for (int32_t k = 0; k < C; ++k) acc += e[i * C + k] * O[(size_t)k * D + j];
+        dA[(size_t)i * D + j] = acc;
+      }
+  }
+  if (dO != NULL) {
+    for (int32_t k = 0; k < C; ++k)
+      for (int32_t j = 0; j < D; ++j) {
+        double acc = 0.0;
+        for (int32_t i = 0; i < N; ++i) acc += e[i * C + k] * A[(size_t)i * D + j];
+        dO[(size_t)k * D + j] = acc;
+      }
+  }
+  if (loss != NULL) *loss = total_loss;
+  free(x);
+  free(e);
+}
+
+/* Gathers the rows of the minibatch; returns the number of present input
+ * words, or -1 when an id is out of range. rows_in/rows_out receive ids. */
+static int32_t gather(const float* M_in, const float* M_out, int32_t V,
+                      int32_t D, int32_t ld, int32_t N, const int32_t* ctx,
+                      int32_t target, int32_t K, const int32_t* negs,
+                      double* A, double* O, int32_t* rows_in,
+                      int32_t* rows_out) {
+  int32_t n = 0;
+  for (int32_t i = 0; i < N; ++i) {
+    if (ctx[i] < 0) continue;
+    if (ctx[i] >= V) return -1;
+    rows_in[n] = ctx[i];
+    for (int32_t j = 0; j < D; ++j)
+      A[(size_t)n * D + j] = (double)M_in[(size_t)ctx[i] * ld + j];
+    ++n;
+  }
+  for (int32_t k = 0; k <= K; ++k) {
+    int32_t id = (k == 0) ? target : negs[k - 1];
+    if (id < 0 || id >= V) return -1;
+    rows_out[k] = id;
+    for (int32_t j = 0; j < D; ++j)
+      O[(size_t)k * D + j] = (double)M_out[(size_t)id * ld + j];
+  }
+  return n;
+}
+
+/* Sums the update rows per destination id in fp64 and rounds once. */
+static void write_back(float* M, int32_t D, int32_t ld, int32_t n_rows,
+                       const int32_t* rows, const double* dM, double* acc) {
+  for (int32_t r = 0; r < n_rows; ++r) {
+    int first = 1;
+    for (int32_t q = 0; q < r; ++q)
+      if (rows[q] == rows[r]) first = 0;
+    if (!first) continue;
+    for (int32_t j = 0; j < D; ++j) acc[j] = 0.0;
+    for (int32_t q = r; q < n_rows; ++q) {
+      if (rows[q] != rows[r]) continue;
+      for (int32_t j = 0; j < D; ++j) acc[j] += dM[(size_t)q * D + j];
+    }
+    float* row = M + (size_t)rows[r] * ld;
+    for (int32_t j = 0; j < D; ++j) row[j] = (float)((double)row[j] + acc[j]);
+  }
+}
+
+int oracle_apply_minibatch(float* M_in, float* M_out, int32_t V, int32_t D,
+                           int32_t ld, int32_t N, const int32_t* ctx,
+                           int32_t target, int32_t K, const int32_t* negs,
+                           const uint8_t* mask, float alpha, double* loss,
+                           int32_t* n_ctx) {
+  if (M_in == NULL || M_out == NULL || V <= 0 || D <= 0 || ld < D || N < 0 ||
+      K < 0 || (N > 0 && ctx == NULL) || (K > 0 && negs == NULL))
+    return -1;
+  const int32_t C = K + 1;
+  double* A = (double*)malloc(sizeof(double) * (size_t)(N + 1) * D);
+  double* O = (double*)malloc(sizeof(double) * (size_t)C * D);
+  double* dA = (double*)malloc(sizeof(double) * (size_t)(N + 1) * D);
+  double* dO = (double*)malloc(sizeof(double) * (size_t)C * D);
+  double* acc = (double*)malloc(sizeof(double) * (size_t)D);
+  int32_t* rows_in = (int32_t*)malloc(sizeof(int32_t) * (size_t)(N + 1));
+  int32_t* rows_out = (int32_t*)malloc(sizeof(int32_t) * (size_t)C);
+  int status = 0;
+  int32_t n = gather(M_in, M_out, V, D, ld, N, ctx, target, K, negs, A, O,
+                     rows_in, rows_out);
+  if (n < 0) {
+    status = -1;
+  } else if (n > 0) {
+    double l = 0.0;
+    oracle_sgns_delta(n, K, D, A, O, mask, (double)alpha, NULL, dA, dO, &l);
+    write_back(M_in, D, ld, n, rows_in, dA, acc);
+    write_back(M_out, D, ld, C, rows_out, dO, acc);
+    if (loss != NULL) *loss = l;
+  } else if (loss != NULL) {
+    *loss = 0.0;
+  }
+  if (n_ctx != NULL) *n_ctx = n < 0 ? 0 : n;
+  free(A); free(O); free(dA); free(dO); free(acc); free(rows_in); free(rows_out);
+  return status;
+}
+
+int oracle_step_batch(int32_t B, int32_t N, int32_t K, const int32_t* targets,
+                      const int32_t* contexts, const int32_t* negatives,
+                      const float* alpha, float alpha_scalar, float* M_in,
+                      float* M_out, int32_t V, int32_t D, int32_t ld,
+                      double* S_in, double* S_out) {
+  if (B < 0 || N < 0 || K < 0 || V <= 0 || D <= 0 || ld < D ||
+      M_in == NULL || M_out == NULL || (B > 0 && targets == NULL) ||
+      (B > 0 && N > 0 && contexts == NULL) ||
+      (B > 0 && K > 0 && negatives == NULL))
+    return -1;
+  const int32_t C = K + 1;
+  const size_t VD = (size_t)V * (size_t)D;
+  double* dM_in = (double*)calloc(VD, sizeof(double));
+  double* dM_out = (double*)calloc(VD, sizeof(double));
+  uint8_t* touched_in = (uint8_t*)calloc((size_t)V, 1);
+  uint8_t* touched_out = (uint8_t*)calloc((size_t)V, 1);
+  double* A = (double*)malloc(sizeof(double) * (size_t)(N + 1) * D);
+  double* O = (double*)malloc(sizeof(double) * (size_t)C * D);
+  double* dA = (double*)malloc(sizeof(double) * (size_t)(N + 1) * D);
+  double* dO = (double*)malloc(sizeof(double) * (size_t)C * D);
+  int32_t* rows_in = (int32_t*)malloc(sizeof(int32_t) * (size_t)(N + 1));
+  int32_t* rows_out = (int32_t*)malloc(sizeof(int32_t) * (size_t)C);
+  uint8_t* mask = (uint8_t*)malloc((size_t)K + 1);
+  int status = 0;
+  if (!dM_in || !dM_out || !touched_in || !touched_out || !A || !O || !dA ||
+      !dO || !rows_in || !rows_out || !mask) {
+    status = -2;
+    goto done;
+  }
+  if (S_in != NULL)
+    for (int32_t r = 0; r < V; ++r)
+      for (int32_t j = 0; j < D; ++j)
+        S_in[(size_t)r * D + j] = fabs((double)M_in[(size_t)r * ld + j]);
+  if (S_out != NULL)
+    for (int32_t r = 0; r < V; ++r)
+      for (int32_t j = 0; j < D; ++j)
+        S_out[(size_t)r * D + j] = fabs((double)M_out[(size_t)r * ld + j]);
+  /* Validate every id before any arithmetic. */
+  for (int32_t b = 0; b < B; ++b) {
+    if (targets[b] < 0 || targets[b] >= V) { status = -1; goto done; }
+    for (int32_t i = 0; i < N; ++i) {
+      int32_t id = contexts[(size_t)b * N + i];
+      if (id < -1 || id >= V) { status = -1; goto done; }
+    }
+    for (int32_t k = 0; k < K; ++k) {
+      int32_t id = negatives[(size_t)b * K + k];
+      if (id < 0 || id >= V) { status = -1; goto done; }
+    }
+  }
+  for (int32_t b = 0; b < B; ++b) {
+    const int32_t* negs = negatives + (size_t)b * K;
+    for (int32_t k = 0; k < K; ++k) mask[k] = (uint8_t)(negs[k] == targets[b]);
+    int32_t n = gather(M_in, M_out, V, D, ld, N, contexts + (size_t)b * N,
+                       targets[b], K, negs, A, O, rows_in, rows_out);
+    if (n <= 0) continue;
+    double a = alpha != NULL ? (double)alpha[b] : (double)alpha_scalar;
+    oracle_sgns_delta(n, K, D, A, O, mask, a, NULL, dA, dO, NULL);
+    for (int32_t i = 0; i < n; ++i) {
+      size_t base = (size_t)rows_in[i] * D;
+      touched_in[rows_in[i]] = 1;
+      for (int32_t j = 0; j < D; ++j) {
+        double g = dA[(size_t)i * D + j];
+        dM_in[base + j] += g;
+        if (S_in != NULL) S_in[base + j] += fabs(g);
+      }
+    }
+    for (int32_t k = 0; k < C; ++k) {
+      if (k > 0 && mask[k - 1]) continue; /* masked column: no update */
+      size_t base = (size_t)rows_out[k] * D;
+      touched_out[rows_out[k]] = 1;
+      for (int32_t j = 0; j < D; ++j) {
+        double g = dO[(size_t)k * D + j];
+        dM_out[base + j] += g;
+        if (S_out != NULL) S_out[base + j] += fabs(g);
+      }
+    }
+  }
+  for (int32_t r = 0; r < V; ++r) {
+    if (touched_in[r])
+      for (int32_t j = 0; j < D; ++j) {
+        float* m = M_in + (size_t)r * ld + j;
+        *m = (float)((double)*m + dM_in[(size_t)r * D + j]);
+      }
+    if (touched_out[r])
+      for (int32_t j = 0; j < D; ++j) {
+        float* m = M_out + (size_t)r * ld + j;
+        *m = (float)((double)*m + dM_out[(size_t)r * D + j]);
+      }
+  }
+done:
+  free(dM_in); free(dM_out); free(touched_in); free(touched_out);
+  free(A); free(O); free(dA); free(dO); free(rows_in); free(rows_out); free(mask);
+  return status;
+}
+
+int64_t oracle_train_epoch(const oracle_sampling* s, float* M_in, float* M_out,
+                           int32_t V, int32_t D, int32_t ld,
+                           double* loss_buckets, int32_t n_buckets) {
+  if (oracle_validate_sampling(s) != 0) return -1;
+  if (M_in == NULL || M_out == NULL || V <= 0 || D <= 0 || ld < D) return -1;
+  if (loss_buckets != NULL && n_buckets <= 0) return -1;
+  oracle_sentence sen;
+  if (oracle_sentence_alloc(&sen, s->sentence_len, s->window, s->K) != 0)
+    return -2;
+  const int32_t w2 = 2 * s->window;
+  int64_t applied = 0;
+  int status = 0;
+  for (int64_t sb = s->pos_begin; sb < s->pos_end && status == 0;
+       sb += s->sentence_len) {
+    int64_t se = sb + s->sentence_len;
+    if (se > s->T) se = s->T;
+    int32_t n_mb = oracle_sentence_minibatches(s, sb, se, &sen);
+    for (int32_t m = 0; m < n_mb; ++m) {
+      double loss = 0.0;
+      int32_t n_ctx = 0;
+      status = oracle_apply_minibatch(
+          M_in, M_out, V, D, ld, w2, sen.ctx + (size_t)m * w2, sen.target[m],
+          s->K, sen.negs + (size_t)m * s->K, sen.mask + (size_t)m * s->K,
+          sen.alpha[m], &loss, &n_ctx);
+      if (status != 0) break;
+      if (loss_buckets != NULL) {
+        int64_t b = sen.pos[m] * (int64_t)n_buckets / s->T;
+        loss_buckets[2 * b] += loss;
+        loss_buckets[2 * b + 1] += (double)n_ctx;
+      }
+      ++applied;
+    }
+  }
+  oracle_sentence_free(&sen);
+  return status == 0 ? applied : -1;
+}
