@@ -61,6 +61,10 @@ def lib():
         L.oracle_sgns_delta.argtypes = [ctypes.c_int32] * 3 + [_f64p, _f64p, _u8p,
                                         ctypes.c_double, _f64p, _f64p, _f64p, _f64p]
         L.oracle_sgns_delta.restype = None
+        L.oracle_sgns_delta_scaled.argtypes = [ctypes.c_int32] * 3 + [
+            _f64p, _f64p, _u8p, ctypes.c_double, _f64p, _f64p, _f64p, _f64p,
+            _f64p, _f64p]
+        L.oracle_sgns_delta_scaled.restype = None
         L.oracle_apply_minibatch.argtypes = [
             _f32p, _f32p, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
             ctypes.c_int32, _i32p, ctypes.c_int32, ctypes.c_int32, _i32p, _u8p,
@@ -186,6 +190,28 @@ def sgns_delta(A, O, mask, alpha):
     return X, dA, dO, loss.value
 
 
+def sgns_delta_scaled(A, O, mask, alpha):
+    """sgns_delta plus the per-element error scales: (X, dA, dO, loss, sA, sO)
+    with sA = |E| |O| and sO = |E|^T |A|."""
+    A = _c(A, np.float64)
+    O = _c(O, np.float64)
+    N, D = A.shape
+    K = O.shape[0] - 1
+    mask = _c(mask if mask is not None else np.zeros(K, np.uint8), np.uint8)
+    X = np.empty((N, K + 1))
+    dA = np.empty((N, D))
+    dO = np.empty((K + 1, D))
+    sA = np.empty((N, D))
+    sO = np.empty((K + 1, D))
+    loss = ctypes.c_double()
+    lib().oracle_sgns_delta_scaled(N, K, D, _ptr(A, _f64p), _ptr(O, _f64p),
+                                   _ptr(mask, _u8p), float(alpha), _ptr(X, _f64p),
+                                   _ptr(dA, _f64p), _ptr(dO, _f64p),
+                                   ctypes.byref(loss), _ptr(sA, _f64p),
+                                   _ptr(sO, _f64p))
+    return X, dA, dO, loss.value, sA, sO
+
+
 def apply_minibatch(M_in, M_out, ctx, target, negs, alpha, mask=None):
     """Applies one minibatch in place to fp32 matrices; returns (loss, n_ctx)."""
     assert M_in.dtype == np.float32 and M_in.flags.c_contiguous
@@ -213,7 +239,8 @@ def step_batch(targets, contexts, negatives, M_in, M_out, alpha=0.025,
     """Snapshot batch: returns (M_in', M_out', S_in, S_out) as new arrays.
 
     alpha is a scalar or an array of B learning rates. S_* are the per-element
-    |M0| + sum |per-occurrence update| (None when with_scale is False).
+    error scales |M0| + sum over occurrences of sum |products| (None when
+    with_scale is False).
     """
     targets = _c(targets, np.int32)
     contexts = _c(contexts, np.int32)

@@ -91,6 +91,15 @@ void oracle_sgns_delta(int32_t N, int32_t K, int32_t D, const double* A,
                        const double* O, const uint8_t* mask, double alpha,
                        double* X, double* dA, double* dO, double* loss);
 
+/* oracle_sgns_delta plus the rounding-error scale of each update element:
+ * sA[i][j] = sum_k |E_ik| |O_kj| and sO[k][j] = sum_i |E_ik| |A_ij| (the sums
+ * of absolute products whose fp32 evaluation the GPU performs). sA, sO may be
+ * NULL. */
+void oracle_sgns_delta_scaled(int32_t N, int32_t K, int32_t D, const double* A,
+                              const double* O, const uint8_t* mask,
+                              double alpha, double* X, double* dA, double* dO,
+                              double* loss, double* sA, double* sO);
+
 /* Applies one minibatch to fp32 matrices in place: the gradients are computed
  * from the current (pre-update) rows, summed per destination row in fp64 and
  * rounded to fp32 once per element. ctx has N entries (-1 = absent). */
@@ -104,9 +113,11 @@ int oracle_apply_minibatch(float* M_in, float* M_out, int32_t V, int32_t D,
  * input matrices, all updates summed in fp64 and rounded once at the end.
  * contexts [B][N] (-1 = absent), negatives [B][K]; a negative equal to its
  * target is masked. alpha is [B] or NULL (then alpha_scalar for all).
- * If S_in / S_out (V x D doubles, row stride D) are non-NULL they receive
- * |M0| + sum of |per-occurrence update| per element (the scale of the
- * rounding-error bound). */
+ * If S_in / S_out (V x D doubles, row stride D) are non-NULL they receive,
+ * per element, |M0| plus, over every occurrence of the row in the batch, the
+ * sum of absolute products forming that occurrence's update (sA / sO of
+ * oracle_sgns_delta_scaled): the scale of the rounding error of evaluating
+ * the update in fp32. */
 int oracle_step_batch(int32_t B, int32_t N, int32_t K, const int32_t* targets,
                       const int32_t* contexts, const int32_t* negatives,
                       const float* alpha, float alpha_scalar, float* M_in,

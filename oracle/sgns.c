@@ -39,6 +39,14 @@ static double log_sigma(double x) {
 void oracle_sgns_delta(int32_t N, int32_t K, int32_t D, const double* A,
                        const double* O, const uint8_t* mask, double alpha,
                        double* X, double* dA, double* dO, double* loss) {
+  oracle_sgns_delta_scaled(N, K, D, A, O, mask, alpha, X, dA, dO, loss, NULL,
+                           NULL);
+}
+
+void oracle_sgns_delta_scaled(int32_t N, int32_t K, int32_t D, const double* A,
+                              const double* O, const uint8_t* mask,
+                              double alpha, double* X, double* dA, double* dO,
+                              double* loss, double* sA, double* sO) {
   const int32_t C = K + 1;
   double* x = (double*)malloc(sizeof(double) * (size_t)(N * C + 1));
   double* e = (double*)malloc(sizeof(double) * (size_t)(N * C + 1));
@@ -69,6 +77,24 @@ void oracle_sgns_delta(int32_t N, int32_t K, int32_t D, const double* A,
         double acc = 0.0;
         for (int32_t i = 0; i < N; ++i) acc += e[i * C + k] * A[(size_t)i * D + j];
         dO[(size_t)k * D + j] = acc;
+      }
+  }
+  if (sA != NULL) {
+    for (int32_t i = 0; i < N; ++i)
+      for (int32_t j = 0; j < D; ++j) {
+        double acc = 0.0;
+        for (int32_t k = 0; k < C; ++k)
+          acc += fabs(e[i * C + k]) * fabs(O[(size_t)k * D + j]);
+        sA[(size_t)i * D + j] = acc;
+      }
+  }
+  if (sO != NULL) {
+    for (int32_t k = 0; k < C; ++k)
+      for (int32_t j = 0; j < D; ++j) {
+        double acc = 0.0;
+        for (int32_t i = 0; i < N; ++i)
+          acc += fabs(e[i * C + k]) * fabs(A[(size_t)i * D + j]);
+        sO[(size_t)k * D + j] = acc;
       }
   }
   if (loss != NULL) *loss = total_loss;
@@ -175,12 +201,14 @@ int oracle_step_batch(int32_t B, int32_t N, int32_t K, const int32_t* targets,
   double* O = (double*)malloc(sizeof(double) * (size_t)C * D);
   double* dA = (double*)malloc(sizeof(double) * (size_t)(N + 1) * D);
   double* dO = (double*)malloc(sizeof(double) * (size_t)C * D);
+  double* sA = (double*)malloc(sizeof(double) * (size_t)(N + 1) * D);
+  double* sO = (double*)malloc(sizeof(double) * (size_t)C * D);
   int32_t* rows_in = (int32_t*)malloc(sizeof(int32_t) * (size_t)(N + 1));
   int32_t* rows_out = (int32_t*)malloc(sizeof(int32_t) * (size_t)C);
   uint8_t* mask = (uint8_t*)malloc((size_t)K + 1);
   int status = 0;
   if (!dM_in || !dM_out || !touched_in || !touched_out || !A || !O || !dA ||
-      !dO || !rows_in || !rows_out || !mask) {
+      !dO || !sA || !sO || !rows_in || !rows_out || !mask) {
     status = -2;
     goto done;
   }
@@ -211,14 +239,14 @@ int oracle_step_batch(int32_t B, int32_t N, int32_t K, const int32_t* targets,
                        targets[b], K, negs, A, O, rows_in, rows_out);
     if (n <= 0) continue;
     double a = alpha != NULL ? (double)alpha[b] : (double)alpha_scalar;
-    oracle_sgns_delta(n, K, D, A, O, mask, a, NULL, dA, dO, NULL);
+    oracle_sgns_delta_scaled(n, K, D, A, O, mask, a, NULL, dA, dO, NULL, sA,
+                             sO);
     for (int32_t i = 0; i < n; ++i) {
       size_t base = (size_t)rows_in[i] * D;
       touched_in[rows_in[i]] = 1;
       for (int32_t j = 0; j < D; ++j) {
-        double g = dA[(size_t)i * D + j];
-        dM_in[base + j] += g;
-        if (S_in != NULL) S_in[base + j] += fabs(g);
+        dM_in[base + j] += dA[(size_t)i * D + j];
+        if (S_in != NULL) S_in[base + j] += sA[(size_t)i * D + j];
       }
     }
     for (int32_t k = 0; k < C; ++k) {
@@ -226,9 +254,8 @@ int oracle_step_batch(int32_t B, int32_t N, int32_t K, const int32_t* targets,
       size_t base = (size_t)rows_out[k] * D;
       touched_out[rows_out[k]] = 1;
       for (int32_t j = 0; j < D; ++j) {
-        double g = dO[(size_t)k * D + j];
-        dM_out[base + j] += g;
-        if (S_out != NULL) S_out[base + j] += fabs(g);
+        dM_out[base + j] += dO[(size_t)k * D + j];
+        if (S_out != NULL) S_out[base + j] += sO[(size_t)k * D + j];
       }
     }
   }
@@ -246,7 +273,8 @@ int oracle_step_batch(int32_t B, int32_t N, int32_t K, const int32_t* targets,
   }
 done:
   free(dM_in); free(dM_out); free(touched_in); free(touched_out);
-  free(A); free(O); free(dA); free(dO); free(rows_in); free(rows_out); free(mask);
+  free(A); free(O); free(dA); free(dO); free(sA); free(sO); free(rows_in);
+  free(rows_out); free(mask);
   return status;
 }
 
