@@ -1,0 +1,199 @@
+"""Throughput benchmark of the HogBatch epoch on one MI355X.
+
+Workload (large-vocabulary throughput configuration): a seeded i.i.d.
+Zipf(1.07) corpus of 10^9 word ids over V = 1,000,000 words (standing in for
+the one-billion-word benchmark of the paper's Sec. 2), D = 300 fp32,
+window 5, K = 5 shared negatives from unigram^0.75, subsampling t = 1e-4,
+alpha 0.025 decaying linearly. One step = one w2v_train_epoch over the whole
+corpus (every kernel of the path, inputs already resident in HBM).
+
+Prints one JSON line: Mwords/s (raw corpus words per second, before
+subsampling), the roofline of the epoch kernel from HIP events recorded on its
+stream, and the CPU oracle's rate on a bounded sample of the same workload.
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0   # MI355X HBM3E, 8 TB/s
+METRIC = "Mwords/sec at V=1M D=300 K=5 window=5 (1 GPU); achieved HBM GB/s"
+KERNEL_SOURCES = ["device_common.h", "sgns_core.h", "kernel_args.h",
+                  "epoch_kernels.hip"]
+
+
+def kernel_hash():
+    h = hashlib.sha256()
+    for name in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, "paper_1611_06172_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(path, n_launch_bytes_scale):
+    """HBM bytes per launch from a committed counter summary, if it was taken
+    on the current kernel sources (else None)."""
+    try:
+        with open(path) as f:
+            d = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if d.get("kernel_hash") != kernel_hash():
+        return None
+    return d.get("hbm_bytes_per_launch")
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--tokens", type=float, default=1e9)
+    ap.add_argument("--vocab", type=int, default=1_000_000)
+    ap.add_argument("--dim", type=int, default=300)
+    ap.add_argument("--negative", type=int, default=5)
+    ap.add_argument("--window", type=int, default=5)
+    ap.add_argument("--sample", type=float, default=1e-4)
+    ap.add_argument("--max-inflight", type=int, default=0)
+    ap.add_argument("--cpu-sample-tokens", type=int, default=1_000_000)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--traffic-json",
+                    default=os.path.join(ROOT, "profiles", "k_epoch_traffic.json"))
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(see the sharding design); run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_1611_06172_amd import inputs, w2v
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    V, D, K, W = args.vocab, args.dim, args.negative, args.window
+    T = int(args.tokens)
+    L = 1000
+
+    t0 = time.time()
+    corpus = inputs.zipf_corpus_device(T, V, 1.07, 6, dev)
+    counts = torch.bincount(corpus, minlength=V).cpu().numpy().astype(np.int64)
+    table_h, thr_h = w2v.build_tables(counts, 0.75, args.sample, 10**8)
+    table = torch.from_numpy(table_h).to(dev)
+    thr = torch.from_numpy(thr_h.view(np.int32)).to(dev)
+    M_in0 = inputs.init_matrix(V, D, "uniform", 2)
+    M_in = torch.from_numpy(M_in0).to(dev)
+    M_out = torch.zeros((V, D), dtype=torch.float32, device=dev)
+    stats = torch.zeros(4, dtype=torch.int64, device=dev)
+    torch.cuda.synchronize()
+    print(f"[bench] setup {time.time() - t0:.1f}s: T={T} V={V} D={D} K={K} w={W}",
+          file=sys.stderr, flush=True)
+
+    n_epochs = args.warmup + args.steps
+
+    def step(i):
+        w2v.train_epoch(corpus, M_in, M_out, table, thr, window=W, K=K,
+                        alpha0=0.025, min_alpha_frac=1e-4, epoch=i,
+                        n_epochs=n_epochs, seed=1234, sentence_len=L,
+                        stats=stats, max_inflight=args.max_inflight)
+
+    for i in range(args.warmup):
+        step(i)
+        torch.cuda.synchronize()
+        print(f"[bench] warmup {i} done", file=sys.stderr, flush=True)
+
+    stream = torch.cuda.current_stream()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(args.steps)]
+    stats.zero_()
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for i in range(args.steps):
+        evs[i][0].record(stream)
+        step(args.warmup + i)
+        evs[i][1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_start
+    kern_ms = [a.elapsed_time(b) for a, b in evs]
+    st = stats.cpu().numpy().astype(np.float64) / args.steps
+    print(f"[bench] timed {args.steps} steps in {wall:.2f}s; per launch "
+          f"{[round(x, 1) for x in kern_ms]} ms", file=sys.stderr, flush=True)
+
+    ms_per_step = wall * 1e3 / args.steps
+    words_per_s = T / (wall / args.steps)
+    # Algorithmic bytes per launch: every minibatch gathers and writes back its
+    # N + K + 1 rows (8 D bytes per row) and reads K table entries; every raw
+    # word reads its id and its keep threshold.
+    n_mb, sum_n, raw = st[0], st[1], st[2]
+    alg_bytes = 8.0 * D * (sum_n + n_mb * (K + 1)) + 4.0 * K * n_mb + 8.0 * raw
+    avg_kern_s = float(np.mean(kern_ms)) / 1e3
+    achieved = alg_bytes / avg_kern_s / 1e9
+    traffic = measured_traffic(args.traffic_json, 1.0)
+
+    result = {
+        "metric": METRIC,
+        "value": round(words_per_s / 1e6, 3),
+        "unit": "Mwords/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": (f"large-vocab HogBatch epoch: i.i.d. Zipf(1.07) corpus, "
+                         f"T={T}, V={V}, D={D}, K={K}, window={W}, sample={args.sample}, "
+                         f"sentence {L}, alpha 0.025 linear"),
+            "V": V, "T": T, "D": D, "K": K, "window": W, "sample": args.sample,
+            "minibatches_per_step": int(n_mb), "mean_inputs_per_minibatch":
+                round(sum_n / max(n_mb, 1), 4), "retained_fraction": round(n_mb / raw, 4),
+        },
+        "roofline": {
+            "bound": "hbm",
+            "kernel": "k_epoch",
+            "achieved": round(achieved, 1),
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4),
+            "traffic": traffic,
+            "alg_bytes_per_launch": alg_bytes,
+            "kernel_ms": round(avg_kern_s * 1e3, 3),
+        },
+    }
+
+    if not args.no_cpu_baseline:
+        import oracle
+        n_s = args.cpu_sample_tokens
+        sample_corpus = corpus[:n_s].cpu().numpy()
+        o_in = M_in0.copy()
+        o_out = np.zeros((V, D), dtype=np.float32)
+        s = oracle.Sampling(sample_corpus, table_h, thr_h, window=W, K=K,
+                            sentence_len=L, seed=1234)
+        c0 = time.perf_counter()
+        n_o, _ = oracle.train_epoch(s, o_in, o_out)
+        c_dt = time.perf_counter() - c0
+        result["cpu_baseline"] = {
+            "value": round(n_s / c_dt / 1e6, 5),
+            "unit": "Mwords/s",
+            "cores": 1,
+            "kind": "oracle",
+            "sample": (f"first {n_s} tokens of the same corpus as a 1-epoch run "
+                       f"({n_o} minibatches, same tables and initial M_in), "
+                       f"single-threaded fp64 oracle, {c_dt:.1f}s; host has "
+                       f"{os.cpu_count()} logical CPUs"),
+        }
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,187 @@
+/*
+ * libw2v: HogBatch skip-gram negative-sampling SGD on MI355X (gfx950).
+ *
+ * Implements the shared-memory hot path of Ji, Satish, Li and Dubey,
+ * "Parallelizing Word2Vec in Multi-Core and Many-Core Architectures"
+ * (arXiv 1611.06172): for every target word, one minibatch of N input
+ * (context) words and K negatives shared by those N words (Sec. 1.1, negative
+ * sample sharing), whose dot products form an N x (K+1) block computed as one
+ * small matrix product; the sigmoid error of Alg. 1 and both gradient
+ * products follow, and the model updates are written back Hogwild-style (no
+ * locks, conflicts between concurrent minibatches tolerated; Sec. 1.1,
+ * "HogBatch").
+ *
+ * Conventions for every entry point:
+ *   - M_in and M_out are V x D fp32 matrices, row-major, row stride ld >= D
+ *     (floats). Word w is row w (Alg. 1: M_in holds input-word vectors, M_out
+ *     output-word vectors). Columns D..ld-1 are never read or written.
+ *   - "device" pointers are GPU global memory of the current HIP device;
+ *     "host" pointers are ordinary CPU memory. The caller owns every buffer;
+ *     the library keeps no pointer after a call returns and allocates no
+ *     device memory.
+ *   - GPU entry points are asynchronous on `stream` (a hipStream_t; NULL is
+ *     the null stream). Results are visible once the caller synchronises it.
+ *   - Return value: W2V_OK (0) or a negative W2V_E* code; w2v_last_error()
+ *     then describes the failure. Arguments are validated on the host before
+ *     any HIP call; a call that fails validation launches nothing.
+ *   - Ids read from device memory (corpus, tables, batches) are checked on the
+ *     device: a minibatch that would touch a row outside [0, V) is skipped and
+ *     counted in the optional stats output; no memory outside the given
+ *     buffers is ever accessed.
+ *
+ * Readings of points the paper leaves open (sentence cut, window shrink,
+ * subsampling rule, negative distribution, learning-rate decay, random
+ * numbers) are stated beside each entry point.
+ */
+#ifndef W2V_H
+#define W2V_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define W2V_OK 0
+#define W2V_EINVAL (-1)      /* an argument is out of range or NULL */
+#define W2V_EHIP (-2)        /* the HIP runtime reported an error */
+#define W2V_ENOMEM (-3)      /* a host allocation failed */
+#define W2V_EUNSUPPORTED (-4)/* valid arguments outside the compiled shapes */
+
+/* Shape limits of the compiled kernels. */
+#define W2V_MAX_DIM 640          /* D */
+#define W2V_MAX_WINDOW 16        /* window: up to 2*window input words */
+#define W2V_MAX_NEGATIVE 64      /* K */
+#define W2V_MAX_SENTENCE 1024    /* sentence_len */
+#define W2V_MAX_BATCH_INPUTS 32  /* N of w2v_step_batch */
+
+/* Version of this ABI (major * 100 + minor). */
+int w2v_version(void);
+
+/* Message of the last failed call on this thread ("" if none). The pointer
+ * stays valid until the next call on the same thread. */
+const char* w2v_last_error(void);
+
+/*
+ * Sampling tables from unigram counts (host only; no HIP call).
+ * Paper: Sec. 2 trains with 5 negative samples and sample = 1e-4; Alg. 1
+ * draws each negative "from V". Readings:
+ *   neg_table (host out, int32[table_size], may be NULL): word w owns slots
+ *     [bound(w-1), bound(w)), bound(-1) = 0, bound(V-1) = table_size and
+ *     bound(w) = floor(S_w / S_{V-1} * table_size) with
+ *     S_w = sum_{v <= w} counts[v]^neg_power, summed left to right in fp64
+ *     (neg_power = 0.75 gives the unigram^0.75 distribution).
+ *   keep_thresh (host out, uint32[V], may be NULL): with f = counts[w] /
+ *     sum(counts) and p = sqrt(t/f) + t/f, a position holding w is kept iff
+ *     its 32-bit draw r <= keep_thresh[w]; keep_thresh[w] = 0xFFFFFFFF when
+ *     t == 0, counts[w] == 0 or p >= 1, else max(floor(p * 2^32) - 1, 0).
+ * counts: host int64[V], all >= 0 with a positive sum. table_size in
+ * [1, 2^32). sample_t >= 0.
+ */
+int w2v_build_tables(const int64_t* counts, int32_t V, double neg_power,
+                     double sample_t, int32_t* neg_table, int64_t table_size,
+                     uint32_t* keep_thresh);
+
+/*
+ * One Hogwild epoch (or a sentence-aligned part of one) of HogBatch SGD,
+ * updating M_in and M_out in place on the GPU.
+ *
+ * Minibatch formation (readings; every random decision is a pure function of
+ * (seed, raw position p, epoch) through Philox4x64-10, Salmon et al. SC'11,
+ * with counter (p, epoch, j, 0) and key (seed, 0); block j's four 64-bit
+ * outputs give 32-bit words 8j..8j+7, low half first):
+ *   - the corpus is cut into sentences of sentence_len raw tokens (the last
+ *     may be shorter); windows never cross a sentence;
+ *   - position p is kept iff keep_thresh == NULL or word 0 <= keep_thresh[x_p];
+ *   - each kept word (retained index q in its sentence) is a target; with
+ *     b = floor(word1 * window / 2^32) and h = window - b its input words are
+ *     the kept words at retained indices q-h..q+h except q; a target with no
+ *     input word forms no minibatch;
+ *   - negative k (k < K) is neg_table[floor(word(2+k) * table_size / 2^32)];
+ *     a negative equal to the target is masked (contributes nothing);
+ *   - alpha = fp32(alpha0 * max(min_alpha_frac, 1 - (epoch*T + p) /
+ *     (n_epochs*T))), evaluated in IEEE fp64.
+ * Minibatch step (Sec. 1.1, Alg. 1 error and update directions): with A the
+ * input-word rows of M_in and O = [target row; negative rows] of M_out,
+ *   X = A O^T, E = alpha * (l - sigma(X)), l = (1, 0, ..., 0),
+ *   M_in[input words] += E O, M_out[target, negatives] += E^T A,
+ * all from the rows as read at the start of the minibatch, written back with
+ * fp32 atomic adds. Minibatches of one sentence run in order on one
+ * wavefront; up to max_inflight sentences run concurrently and their updates
+ * interleave without locks (Hogwild). max_inflight = 1 processes every
+ * minibatch in sequence; 0 picks enough concurrent sentences to fill the GPU.
+ *
+ * corpus: device int32[T]. [pos_begin, pos_end) must start on a sentence
+ * boundary and end on one or at T. M_in, M_out: device, see conventions.
+ * neg_table: device int32[table_size]. keep_thresh: device uint32[V] or NULL.
+ * loss_buckets: device double[2 * n_buckets] or NULL; for a minibatch of
+ * target position p, bucket b = floor(p * n_buckets / T) receives
+ * [2b] += sum_i [-log sigma(X_i0) - sum_{k unmasked} log sigma(-X_ik)] and
+ * [2b+1] += N. stats: device int64[4] or NULL, accumulated into:
+ * [0] minibatches applied, [1] sum of N over them, [2] raw positions
+ * visited, [3] minibatches skipped for an id outside [0, V).
+ * Limits: 1 <= D <= W2V_MAX_DIM, 1 <= window <= W2V_MAX_WINDOW,
+ * 0 <= K <= W2V_MAX_NEGATIVE, 1 <= sentence_len <= W2V_MAX_SENTENCE.
+ */
+int w2v_train_epoch(const int32_t* corpus, int64_t T, int64_t pos_begin,
+                    int64_t pos_end, int32_t sentence_len, float* M_in,
+                    float* M_out, int32_t V, int32_t D, int32_t ld,
+                    int32_t window, int32_t K, const int32_t* neg_table,
+                    int64_t table_size, const uint32_t* keep_thresh,
+                    float alpha0, float min_alpha_frac, int32_t epoch,
+                    int32_t n_epochs, uint64_t seed, double* loss_buckets,
+                    int32_t n_buckets, int64_t* stats, int32_t max_inflight,
+                    void* stream);
+
+/*
+ * The minibatches w2v_train_epoch would form over [pos_begin, pos_end),
+ * written out instead of applied (same arguments and readings as
+ * w2v_train_epoch; the matrices are not needed). Outputs are indexed by raw
+ * position r = p - pos_begin, P = pos_end - pos_begin:
+ *   out_targets  device int32[P]: the target word, or -1 where position p
+ *                forms no minibatch (not kept, or no input word);
+ *   out_ctx      device int32[P][2*window]: input words in order, -1 padded;
+ *   out_negs     device int32[P][K]; out_mask device uint8[P][K];
+ *   out_alpha    device float[P].
+ * Entries of out_ctx/out_negs/out_mask/out_alpha are written only where
+ * out_targets != -1. stats as in w2v_train_epoch (may be NULL).
+ */
+int w2v_debug_minibatches(const int32_t* corpus, int64_t T, int64_t pos_begin,
+                          int64_t pos_end, int32_t sentence_len, int32_t V,
+                          int32_t window, int32_t K, const int32_t* neg_table,
+                          int64_t table_size, const uint32_t* keep_thresh,
+                          float alpha0, float min_alpha_frac, int32_t epoch,
+                          int32_t n_epochs, uint64_t seed, int32_t* out_targets,
+                          int32_t* out_ctx, int32_t* out_negs,
+                          uint8_t* out_mask, float* out_alpha, int64_t* stats,
+                          void* stream);
+
+/* Bytes of workspace w2v_step_batch needs: two fp64 V x ld delta buffers. */
+size_t w2v_step_batch_workspace_bytes(int32_t V, int32_t ld);
+
+/*
+ * One deterministic batch of B independent HogBatch minibatches against given
+ * matrices: every gradient is computed from the matrices as they were on
+ * entry; the per-minibatch updates are summed per element in fp64 (in
+ * `workspace`) and each touched element becomes fp32(M + sum), one rounding
+ * per element. Elements whose summed update is exactly 0 keep their bits.
+ * targets: device int32[B]; contexts: device int32[B][N], -1 = absent;
+ * negatives: device int32[B][K]; a negative equal to its target is masked.
+ * alpha: device float[B], or NULL to use alpha_scalar for every minibatch.
+ * workspace: device, >= w2v_step_batch_workspace_bytes(V, ld) bytes, 256-byte
+ * aligned. stats: device int64[4] or NULL, as in w2v_train_epoch.
+ * Limits: 0 <= N <= W2V_MAX_BATCH_INPUTS, 0 <= K <= W2V_MAX_NEGATIVE,
+ * 1 <= D <= W2V_MAX_DIM.
+ */
+int w2v_step_batch(int32_t B, int32_t N, int32_t K, const int32_t* targets,
+                   const int32_t* contexts, const int32_t* negatives,
+                   const float* alpha, float alpha_scalar, float* M_in,
+                   float* M_out, int32_t V, int32_t D, int32_t ld,
+                   void* workspace, size_t workspace_bytes, int64_t* stats,
+                   void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

@@ -1,0 +1,290 @@
+// C ABI of libw2v (declared in include/w2v.h): argument validation, error
+// reporting and kernel launches. Every check runs on the host before any HIP
+// call, so a rejected call has no device side effect.
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <mutex>
+
+#include "kernel_args.h"
+#include "w2v_internal.h"
+
+namespace w2v {
+
+static thread_local char g_error[512] = "";
+
+int fail(int code, const char* msg) {
+  snprintf(g_error, sizeof(g_error), "%s", msg);
+  return code;
+}
+
+int failf(int code, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_error, sizeof(g_error), fmt, ap);
+  va_end(ap);
+  return code;
+}
+
+int ok() {
+  g_error[0] = '\0';
+  return W2V_OK;
+}
+
+static int hip_fail(hipError_t e, const char* what) {
+  return failf(W2V_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+// Compute units of the current device (queried once per device).
+static int cu_count() {
+  static std::mutex mu;
+  static int cached[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+  std::lock_guard<std::mutex> lock(mu);
+  if (cached[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) ==
+        hipSuccess)
+      cached[dev] = n;
+  }
+  return cached[dev];
+}
+
+struct SamplingCheck {
+  const int32_t* corpus;
+  int64_t T, pos_begin, pos_end;
+  int32_t L, V, window, K;
+  const int32_t* table;
+  int64_t table_size;
+  int32_t epoch, n_epochs;
+};
+
+static int check_sampling(const SamplingCheck& c) {
+  if (c.corpus == nullptr) return fail(W2V_EINVAL, "corpus is NULL");
+  if (c.table == nullptr) return fail(W2V_EINVAL, "neg_table is NULL");
+  if (c.T <= 0) return fail(W2V_EINVAL, "T must be positive");
+  if (c.L < 1 || c.L > W2V_MAX_SENTENCE)
+    return failf(W2V_EINVAL, "sentence_len must be in [1, %d]", W2V_MAX_SENTENCE);
+  if (c.pos_begin < 0 || c.pos_end > c.T || c.pos_begin > c.pos_end)
+    return fail(W2V_EINVAL, "need 0 <= pos_begin <= pos_end <= T");
+  if (c.pos_begin % c.L != 0)
+    return fail(W2V_EINVAL, "pos_begin must start a sentence");
+  if (c.pos_end != c.T && c.pos_end % c.L != 0)
+    return fail(W2V_EINVAL, "pos_end must end a sentence or equal T");
+  if (c.V <= 0) return fail(W2V_EINVAL, "V must be positive");
+  if (c.window < 1 || c.window > W2V_MAX_WINDOW)
+    return failf(W2V_EINVAL, "window must be in [1, %d]", W2V_MAX_WINDOW);
+  if (c.K < 0 || c.K > W2V_MAX_NEGATIVE)
+    return failf(W2V_EINVAL, "K must be in [0, %d]", W2V_MAX_NEGATIVE);
+  if (c.table_size <= 0 || c.table_size >= (int64_t(1) << 32))
+    return fail(W2V_EINVAL, "table_size must be in [1, 2^32)");
+  if (c.n_epochs < 1 || c.epoch < 0 || c.epoch >= c.n_epochs)
+    return fail(W2V_EINVAL, "need 0 <= epoch < n_epochs");
+  return W2V_OK;
+}
+
+static int check_matrices(const float* M_in, const float* M_out, int32_t V,
+                          int32_t D, int32_t ld) {
+  if (M_in == nullptr || M_out == nullptr)
+    return fail(W2V_EINVAL, "M_in and M_out must not be NULL");
+  if (V <= 0) return fail(W2V_EINVAL, "V must be positive");
+  if (D < 1 || D > W2V_MAX_DIM)
+    return failf(W2V_EINVAL, "D must be in [1, %d]", W2V_MAX_DIM);
+  if (ld < D) return fail(W2V_EINVAL, "ld must be >= D");
+  return W2V_OK;
+}
+
+}  // namespace w2v
+
+using namespace w2v;
+
+extern "C" {
+
+int w2v_version(void) { return 100; }
+
+const char* w2v_last_error(void) { return g_error; }
+
+int w2v_build_tables(const int64_t* counts, int32_t V, double neg_power,
+                     double sample_t, int32_t* neg_table, int64_t table_size,
+                     uint32_t* keep_thresh) {
+  return build_tables(counts, V, neg_power, sample_t, neg_table, table_size,
+                      keep_thresh);
+}
+
+int w2v_train_epoch(const int32_t* corpus, int64_t T, int64_t pos_begin,
+                    int64_t pos_end, int32_t sentence_len, float* M_in,
+                    float* M_out, int32_t V, int32_t D, int32_t ld,
+                    int32_t window, int32_t K, const int32_t* neg_table,
+                    int64_t table_size, const uint32_t* keep_thresh,
+                    float alpha0, float min_alpha_frac, int32_t epoch,
+                    int32_t n_epochs, uint64_t seed, double* loss_buckets,
+                    int32_t n_buckets, int64_t* stats, int32_t max_inflight,
+                    void* stream) {
+  int rc = check_sampling({corpus, T, pos_begin, pos_end, sentence_len, V,
+                           window, K, neg_table, table_size, epoch, n_epochs});
+  if (rc != W2V_OK) return rc;
+  rc = check_matrices(M_in, M_out, V, D, ld);
+  if (rc != W2V_OK) return rc;
+  if (loss_buckets != nullptr && n_buckets < 1)
+    return fail(W2V_EINVAL, "n_buckets must be >= 1 with loss_buckets");
+  if (max_inflight < 0) return fail(W2V_EINVAL, "max_inflight must be >= 0");
+  const int C = columns_for(D);
+  const int nmax = inputs_cap_for(2 * window);
+  if (C == 0 || nmax == 0 || !train_shape_supported(C, nmax))
+    return failf(W2V_EUNSUPPORTED, "no compiled kernel for D=%d window=%d", D,
+                 window);
+  const int64_t n_sent = (pos_end - pos_begin + sentence_len - 1) / sentence_len;
+  if (n_sent == 0) return ok();
+
+  EpochArgs a{};
+  a.corpus = corpus;
+  a.T = T;
+  a.pos_begin = pos_begin;
+  a.pos_end = pos_end;
+  a.n_sent = n_sent;
+  a.L = sentence_len;
+  a.M_in = M_in;
+  a.M_out = M_out;
+  a.V = V;
+  a.D = D;
+  a.ld = ld;
+  a.w = window;
+  a.K = K;
+  a.table = neg_table;
+  a.table_size = table_size;
+  a.thr = keep_thresh;
+  a.alpha0 = alpha0;
+  a.min_frac = min_alpha_frac;
+  a.epoch = epoch;
+  a.n_epochs = n_epochs;
+  a.seed = seed;
+  a.loss = loss_buckets;
+  a.n_buckets = n_buckets;
+  a.stats = stats;
+
+  int64_t grid = max_inflight;
+  if (grid == 0) {
+    const int per_cu = train_blocks_per_cu(C, nmax);
+    const int cus = cu_count();
+    grid = (int64_t)(per_cu > 0 ? per_cu : 1) * (cus > 0 ? cus : 1);
+  }
+  if (grid > n_sent) grid = n_sent;
+  if (grid > (1 << 30)) grid = 1 << 30;
+  hipError_t e = launch_train(C, nmax, a, (int)grid, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "train kernel launch");
+  return ok();
+}
+
+int w2v_debug_minibatches(const int32_t* corpus, int64_t T, int64_t pos_begin,
+                          int64_t pos_end, int32_t sentence_len, int32_t V,
+                          int32_t window, int32_t K, const int32_t* neg_table,
+                          int64_t table_size, const uint32_t* keep_thresh,
+                          float alpha0, float min_alpha_frac, int32_t epoch,
+                          int32_t n_epochs, uint64_t seed, int32_t* out_targets,
+                          int32_t* out_ctx, int32_t* out_negs,
+                          uint8_t* out_mask, float* out_alpha, int64_t* stats,
+                          void* stream) {
+  int rc = check_sampling({corpus, T, pos_begin, pos_end, sentence_len, V,
+                           window, K, neg_table, table_size, epoch, n_epochs});
+  if (rc != W2V_OK) return rc;
+  if (out_targets == nullptr || out_ctx == nullptr || out_alpha == nullptr ||
+      (K > 0 && (out_negs == nullptr || out_mask == nullptr)))
+    return fail(W2V_EINVAL, "output pointers must not be NULL");
+  const int64_t n_sent = (pos_end - pos_begin + sentence_len - 1) / sentence_len;
+  if (n_sent == 0) return ok();
+  EpochArgs a{};
+  a.corpus = corpus;
+  a.T = T;
+  a.pos_begin = pos_begin;
+  a.pos_end = pos_end;
+  a.n_sent = n_sent;
+  a.L = sentence_len;
+  a.V = V;
+  a.D = 1;
+  a.ld = 1;
+  a.w = window;
+  a.K = K;
+  a.table = neg_table;
+  a.table_size = table_size;
+  a.thr = keep_thresh;
+  a.alpha0 = alpha0;
+  a.min_frac = min_alpha_frac;
+  a.epoch = epoch;
+  a.n_epochs = n_epochs;
+  a.seed = seed;
+  a.stats = stats;
+  a.out_targets = out_targets;
+  a.out_ctx = out_ctx;
+  a.out_negs = out_negs;
+  a.out_mask = out_mask;
+  a.out_alpha = out_alpha;
+  int64_t grid = n_sent < (1 << 20) ? n_sent : (1 << 20);
+  hipError_t e = launch_export(a, (int)grid, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "export kernel launch");
+  return ok();
+}
+
+size_t w2v_step_batch_workspace_bytes(int32_t V, int32_t ld) {
+  if (V <= 0 || ld <= 0) return 0;
+  const size_t one = (size_t)V * (size_t)ld * sizeof(double);
+  const size_t aligned = (one + 255) / 256 * 256;
+  return 2 * aligned;
+}
+
+int w2v_step_batch(int32_t B, int32_t N, int32_t K, const int32_t* targets,
+                   const int32_t* contexts, const int32_t* negatives,
+                   const float* alpha, float alpha_scalar, float* M_in,
+                   float* M_out, int32_t V, int32_t D, int32_t ld,
+                   void* workspace, size_t workspace_bytes, int64_t* stats,
+                   void* stream) {
+  if (B < 0) return fail(W2V_EINVAL, "B must be >= 0");
+  if (N < 0 || N > W2V_MAX_BATCH_INPUTS)
+    return failf(W2V_EINVAL, "N must be in [0, %d]", W2V_MAX_BATCH_INPUTS);
+  if (K < 0 || K > W2V_MAX_NEGATIVE)
+    return failf(W2V_EINVAL, "K must be in [0, %d]", W2V_MAX_NEGATIVE);
+  int rc = check_matrices(M_in, M_out, V, D, ld);
+  if (rc != W2V_OK) return rc;
+  if (B > 0 && targets == nullptr) return fail(W2V_EINVAL, "targets is NULL");
+  if (B > 0 && N > 0 && contexts == nullptr)
+    return fail(W2V_EINVAL, "contexts is NULL");
+  if (B > 0 && K > 0 && negatives == nullptr)
+    return fail(W2V_EINVAL, "negatives is NULL");
+  const size_t need = w2v_step_batch_workspace_bytes(V, ld);
+  if (workspace == nullptr || workspace_bytes < need)
+    return failf(W2V_EINVAL, "workspace must hold %zu bytes", need);
+  if (((uintptr_t)workspace & 255u) != 0)
+    return fail(W2V_EINVAL, "workspace must be 256-byte aligned");
+  const int C = columns_for(D);
+  const int nmax = inputs_cap_for(N > 0 ? N : 1);
+  if (C == 0 || nmax == 0 || !train_shape_supported(C, nmax))
+    return failf(W2V_EUNSUPPORTED, "no compiled kernel for D=%d N=%d", D, N);
+  if (B == 0 || N == 0) return ok();
+
+  hipStream_t s = (hipStream_t)stream;
+
+  StepArgs a{};
+  a.B = B;
+  a.N = N;
+  a.K = K;
+  a.targets = targets;
+  a.contexts = contexts;
+  a.negatives = negatives;
+  a.alpha = alpha;
+  a.alpha_scalar = alpha_scalar;
+  a.M_in = M_in;
+  a.dM_in = (double*)workspace;
+  a.dM_out = (double*)((char*)workspace + need / 2);
+  a.M_out = M_out;
+  a.V = V;
+  a.D = D;
+  a.ld = ld;
+  a.stats = stats;
+  const int grid = B < (1 << 20) ? B : (1 << 20);
+  hipError_t e = launch_step(C, nmax, a, grid, s);
+  if (e != hipSuccess) return hip_fail(e, "step kernel launch");
+  return ok();
+}
+
+}  // extern "C"

@@ -1,0 +1,66 @@
+// Argument blocks of the HogBatch kernels and their host launchers.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace w2v {
+
+// Sentence-parallel epoch (training or minibatch export).
+struct EpochArgs {
+  const int32_t* corpus;
+  int64_t T, pos_begin, pos_end;
+  int64_t n_sent;          // sentences in [pos_begin, pos_end)
+  int32_t L;               // sentence length
+  float* M_in;
+  float* M_out;
+  int32_t V, D;
+  int64_t ld;
+  int32_t w, K;
+  const int32_t* table;
+  int64_t table_size;
+  const uint32_t* thr;     // NULL: keep every position
+  float alpha0, min_frac;
+  int32_t epoch, n_epochs;
+  uint64_t seed;
+  double* loss;            // NULL or double[2 * n_buckets]
+  int32_t n_buckets;
+  int64_t* stats;          // NULL or int64[4]
+  // export outputs (minibatch export only)
+  int32_t* out_targets;
+  int32_t* out_ctx;
+  int32_t* out_negs;
+  uint8_t* out_mask;
+  float* out_alpha;
+};
+
+// Snapshot batch of independent minibatches.
+struct StepArgs {
+  int32_t B, N, K;
+  const int32_t* targets;
+  const int32_t* contexts;
+  const int32_t* negatives;
+  const float* alpha;      // NULL: alpha_scalar
+  float alpha_scalar;
+  float* M_in;             // rows read, then updated by the finalize pass
+  float* M_out;
+  double* dM_in;           // fp64 delta buffers (workspace), row stride ld
+  double* dM_out;
+  int32_t V, D;
+  int64_t ld;
+  int64_t* stats;
+};
+
+// Launchers (defined next to the kernels). Return a hipError_t.
+// C: columns per lane (D <= 64 C); nmax: max input words per minibatch.
+hipError_t launch_train(int C, int nmax, const EpochArgs& a, int grid,
+                        hipStream_t s);
+hipError_t launch_export(const EpochArgs& a, int grid, hipStream_t s);
+hipError_t launch_step(int C, int nmax, const StepArgs& a, int grid,
+                       hipStream_t s);
+bool train_shape_supported(int C, int nmax);
+int columns_for(int D);      // compiled C for a row length, 0 if none
+int inputs_cap_for(int n);   // compiled nmax for n input words, 0 if none
+int train_blocks_per_cu(int C, int nmax);
+
+}  // namespace w2v

@@ -1,0 +1,21 @@
+// Host-side internals of libw2v: error state and shared helpers.
+#pragma once
+
+#include <stdint.h>
+
+#include "../../include/w2v.h"
+
+namespace w2v {
+
+// Records `msg` as this thread's last error and returns `code`.
+int fail(int code, const char* msg);
+// Formats a message (printf-style) and records it.
+int failf(int code, const char* fmt, ...);
+// Clears this thread's last error and returns W2V_OK.
+int ok();
+
+int build_tables(const int64_t* counts, int32_t V, double power,
+                 double sample_t, int32_t* table, int64_t table_size,
+                 uint32_t* keep);
+
+}  // namespace w2v

@@ -1,0 +1,242 @@
+"""ctypes binding of libw2v (include/w2v.h): argument marshalling only.
+
+Every function takes torch tensors that already live where the C ABI expects
+them (device tensors on the current HIP device for GPU entry points), checks
+dtypes and shapes, and passes raw pointers plus the current torch stream.
+No arithmetic of the method happens here. If libw2v.so has not been built the
+first call raises: there is no CPU fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libw2v.so")
+
+_vp = ctypes.c_void_p
+_i32 = ctypes.c_int32
+_i64 = ctypes.c_int64
+_f32 = ctypes.c_float
+_f64 = ctypes.c_double
+_u64 = ctypes.c_uint64
+
+_lib = None
+
+OK = 0
+EINVAL = -1
+EHIP = -2
+ENOMEM = -3
+EUNSUPPORTED = -4
+
+
+class W2VError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"libw2v error {code}: {msg}")
+        self.code = code
+
+
+def lib():
+    """The loaded libw2v.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(
+            f"{LIB_PATH} is missing: build it with __graft_entry__.build() "
+            "(hipcc, gfx950) before using the GPU path")
+    L = ctypes.CDLL(LIB_PATH)
+    L.w2v_version.restype = ctypes.c_int
+    L.w2v_last_error.restype = ctypes.c_char_p
+    L.w2v_build_tables.argtypes = [_vp, _i32, _f64, _f64, _vp, _i64, _vp]
+    L.w2v_build_tables.restype = ctypes.c_int
+    L.w2v_train_epoch.argtypes = [
+        _vp, _i64, _i64, _i64, _i32, _vp, _vp, _i32, _i32, _i32, _i32, _i32,
+        _vp, _i64, _vp, _f32, _f32, _i32, _i32, _u64, _vp, _i32, _vp, _i32, _vp]
+    L.w2v_train_epoch.restype = ctypes.c_int
+    L.w2v_debug_minibatches.argtypes = [
+        _vp, _i64, _i64, _i64, _i32, _i32, _i32, _i32, _vp, _i64, _vp, _f32,
+        _f32, _i32, _i32, _u64, _vp, _vp, _vp, _vp, _vp, _vp, _vp]
+    L.w2v_debug_minibatches.restype = ctypes.c_int
+    L.w2v_step_batch_workspace_bytes.argtypes = [_i32, _i32]
+    L.w2v_step_batch_workspace_bytes.restype = ctypes.c_size_t
+    L.w2v_step_batch.argtypes = [
+        _i32, _i32, _i32, _vp, _vp, _vp, _vp, _f32, _vp, _vp, _i32, _i32, _i32,
+        _vp, ctypes.c_size_t, _vp, _vp]
+    L.w2v_step_batch.restype = ctypes.c_int
+    _lib = L
+    return L
+
+
+def _check(rc: int):
+    if rc != OK:
+        raise W2VError(rc, lib().w2v_last_error().decode())
+
+
+def _ptr(t) -> Optional[int]:
+    if t is None:
+        return None
+    return t.data_ptr()
+
+
+def _stream(stream=None) -> int:
+    import torch
+    s = torch.cuda.current_stream() if stream is None else stream
+    return s.cuda_stream
+
+
+def _dev(t, dtype, name, ndim=None):
+    import torch
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError(f"{name} must be a GPU tensor")
+    if isinstance(dtype, tuple):
+        if t.dtype not in dtype:
+            raise TypeError(f"{name} must have dtype in {dtype}, got {t.dtype}")
+    elif t.dtype != dtype:
+        raise TypeError(f"{name} must have dtype {dtype}, got {t.dtype}")
+    if ndim is not None and t.dim() != ndim:
+        raise ValueError(f"{name} must be {ndim}-D")
+    if not t.is_contiguous() and not (t.dim() == 2 and t.stride(1) == 1):
+        raise ValueError(f"{name} must be contiguous")
+    return t
+
+
+def _matrix(M, name):
+    import torch
+    _dev(M, torch.float32, name, 2)
+    if M.stride(1) != 1:
+        raise ValueError(f"{name} must have unit column stride")
+    return M.shape[0], M.stride(0)
+
+
+def version() -> int:
+    return int(lib().w2v_version())
+
+
+def build_tables(counts, neg_power: float = 0.75, sample_t: float = 1e-4,
+                 table_size: int = 10**8, want_table: bool = True,
+                 want_thresh: bool = True):
+    """Host tables: (neg_table int32[table_size], keep_thresh uint32[V])."""
+    counts = np.ascontiguousarray(counts, dtype=np.int64)
+    V = counts.shape[0]
+    table = np.empty(table_size, dtype=np.int32) if want_table else None
+    thr = np.empty(V, dtype=np.uint32) if want_thresh else None
+    _check(lib().w2v_build_tables(
+        counts.ctypes.data, V, float(neg_power), float(sample_t),
+        None if table is None else table.ctypes.data, int(table_size),
+        None if thr is None else thr.ctypes.data))
+    return table, thr
+
+
+def train_epoch(corpus, M_in, M_out, neg_table, keep_thresh=None, *,
+                window: int = 5, K: int = 5, D: Optional[int] = None,
+                alpha0: float = 0.025, min_alpha_frac: float = 1e-4,
+                epoch: int = 0, n_epochs: int = 1, seed: int = 0,
+                pos_begin: int = 0, pos_end: Optional[int] = None,
+                sentence_len: int = 1000, loss_buckets=None, stats=None,
+                max_inflight: int = 0, stream=None):
+    """Hogwild HogBatch epoch over corpus[pos_begin:pos_end], in place."""
+    import torch
+    _dev(corpus, torch.int32, "corpus", 1)
+    V, ld = _matrix(M_in, "M_in")
+    V2, ld2 = _matrix(M_out, "M_out")
+    if (V, ld) != (V2, ld2):
+        raise ValueError("M_in and M_out must have the same shape and stride")
+    D = M_in.shape[1] if D is None else D
+    _dev(neg_table, torch.int32, "neg_table", 1)
+    if keep_thresh is not None:
+        _dev(keep_thresh, (torch.int32, torch.uint32), "keep_thresh", 1)
+        if keep_thresh.numel() != V:
+            raise ValueError("keep_thresh must have V entries")
+    n_b = 0
+    if loss_buckets is not None:
+        _dev(loss_buckets, torch.float64, "loss_buckets", 2)
+        n_b = loss_buckets.shape[0]
+    if stats is not None:
+        _dev(stats, torch.int64, "stats", 1)
+    T = corpus.numel()
+    end = T if pos_end is None else pos_end
+    _check(lib().w2v_train_epoch(
+        _ptr(corpus), T, pos_begin, end, sentence_len, _ptr(M_in), _ptr(M_out),
+        V, D, ld, window, K, _ptr(neg_table), neg_table.numel(),
+        _ptr(keep_thresh), alpha0, min_alpha_frac, epoch, n_epochs, seed,
+        _ptr(loss_buckets), n_b, _ptr(stats), max_inflight, _stream(stream)))
+
+
+def debug_minibatches(corpus, neg_table, keep_thresh=None, *, V: int,
+                      window: int = 5, K: int = 5, alpha0: float = 0.025,
+                      min_alpha_frac: float = 1e-4, epoch: int = 0,
+                      n_epochs: int = 1, seed: int = 0, pos_begin: int = 0,
+                      pos_end: Optional[int] = None, sentence_len: int = 1000,
+                      stats=None, stream=None):
+    """Minibatches the epoch would form, indexed by raw position (GPU)."""
+    import torch
+    _dev(corpus, torch.int32, "corpus", 1)
+    _dev(neg_table, torch.int32, "neg_table", 1)
+    if keep_thresh is not None:
+        _dev(keep_thresh, (torch.int32, torch.uint32), "keep_thresh", 1)
+    T = corpus.numel()
+    end = T if pos_end is None else pos_end
+    P = end - pos_begin
+    dev = corpus.device
+    out = dict(
+        targets=torch.empty(P, dtype=torch.int32, device=dev),
+        ctx=torch.empty((P, 2 * window), dtype=torch.int32, device=dev),
+        negs=torch.empty((P, K), dtype=torch.int32, device=dev),
+        mask=torch.empty((P, K), dtype=torch.uint8, device=dev),
+        alpha=torch.empty(P, dtype=torch.float32, device=dev))
+    _check(lib().w2v_debug_minibatches(
+        _ptr(corpus), T, pos_begin, end, sentence_len, V, window, K,
+        _ptr(neg_table), neg_table.numel(), _ptr(keep_thresh), alpha0,
+        min_alpha_frac, epoch, n_epochs, seed, _ptr(out["targets"]),
+        _ptr(out["ctx"]), _ptr(out["negs"]), _ptr(out["mask"]),
+        _ptr(out["alpha"]), _ptr(stats), _stream(stream)))
+    return out
+
+
+def step_batch_workspace_bytes(V: int, ld: int) -> int:
+    return int(lib().w2v_step_batch_workspace_bytes(V, ld))
+
+
+def alloc_workspace(V: int, ld: int, device="cuda"):
+    """A torch-owned byte buffer large enough for step_batch."""
+    import torch
+    n = step_batch_workspace_bytes(V, ld)
+    return torch.empty(n, dtype=torch.uint8, device=device)
+
+
+def step_batch(targets, contexts, negatives, M_in, M_out, alpha=0.025, *,
+               D: Optional[int] = None, workspace=None, stats=None,
+               stream=None):
+    """One snapshot batch of B minibatches; updates M_in, M_out in place."""
+    import torch
+    _dev(targets, torch.int32, "targets", 1)
+    _dev(contexts, torch.int32, "contexts", 2)
+    _dev(negatives, torch.int32, "negatives", 2)
+    B = targets.shape[0]
+    N = contexts.shape[1]
+    K = negatives.shape[1]
+    if contexts.shape[0] != B or negatives.shape[0] != B:
+        raise ValueError("targets, contexts and negatives disagree on B")
+    V, ld = _matrix(M_in, "M_in")
+    if _matrix(M_out, "M_out") != (V, ld):
+        raise ValueError("M_in and M_out must have the same shape and stride")
+    D = M_in.shape[1] if D is None else D
+    if isinstance(alpha, torch.Tensor):
+        _dev(alpha, torch.float32, "alpha", 1)
+        a_ptr, a_s = _ptr(alpha), 0.0
+    else:
+        a_ptr, a_s = None, float(alpha)
+    if workspace is None:
+        workspace = alloc_workspace(V, ld, M_in.device)
+    if stats is not None:
+        _dev(stats, torch.int64, "stats", 1)
+    _check(lib().w2v_step_batch(
+        B, N, K, _ptr(targets), _ptr(contexts), _ptr(negatives), a_ptr, a_s,
+        _ptr(M_in), _ptr(M_out), V, D, ld, _ptr(workspace),
+        workspace.numel() * workspace.element_size(), _ptr(stats),
+        _stream(stream)))
+    return workspace

@@ -1,0 +1,148 @@
+"""w2v_train_epoch against the oracle's sequential epoch.
+
+* Serialised (max_inflight = 1): one wavefront runs every minibatch in corpus
+  order, the oracle's schedule; the two differ only by fp32 versus fp64
+  rounding, which the test bounds elementwise.
+* Counts: minibatches applied and input words summed equal the oracle's
+  exactly (sampling is bit-exact).
+* Hogwild (all sentences concurrent): statistical agreement of the SGNS loss
+  of the trained model on a fixed evaluation batch, within 2%.
+"""
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_1611_06172_amd import inputs, w2v
+from gpu_util import thresh_dev, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+def tiny_config(T=200_000, V=1000, D=64, seed=1):
+    corpus = inputs.zipf_ids(T, V, 1.0, seed)
+    table, _ = oracle.build_tables(inputs.word_counts(corpus, V), 0.75, 0.0, 10**8,
+                                   want_thresh=False)
+    M_in = inputs.init_matrix(V, D, "uniform", 2)
+    M_out = inputs.init_matrix(V, D, "zeros", 0)
+    return corpus, table, M_in, M_out
+
+
+def gpu_epoch(corpus, table, thr, M_in, M_out, n_buckets=0, **kw):
+    import torch
+    gi, go = to_dev(M_in), to_dev(M_out)
+    stats = torch.zeros(4, dtype=torch.int64, device="cuda")
+    lb = torch.zeros((n_buckets, 2), dtype=torch.float64, device="cuda") if n_buckets else None
+    w2v.train_epoch(to_dev(corpus), gi, go, to_dev(table), thresh_dev(thr),
+                    loss_buckets=lb, stats=stats, **kw)
+    torch.cuda.synchronize()
+    return (gi.cpu().numpy(), go.cpu().numpy(), stats.cpu().numpy(),
+            None if lb is None else lb.cpu().numpy())
+
+
+def rel_row_error(g, o):
+    """max over elements of |g - o| / (max |o| in the row + 1e-3 * max |o|)."""
+    d = np.abs(g.astype(np.float64) - o)
+    scale = np.abs(o).max(axis=1, keepdims=True) + 1e-3 * np.abs(o).max()
+    return float((d / scale).max())
+
+
+def test_serialised_epoch_matches_oracle():
+    corpus, table, M_in, M_out = tiny_config(T=60_000)
+    kw = dict(window=5, K=5, sentence_len=1000, seed=7, alpha0=0.025)
+    o_in, o_out = M_in.copy(), M_out.copy()
+    n, ob = oracle.train_epoch(oracle.Sampling(corpus, table, None, **kw), o_in, o_out,
+                               n_buckets=4)
+    gi, go, stats, gb = gpu_epoch(corpus, table, None, M_in, M_out, n_buckets=4,
+                                  max_inflight=1, **kw)
+    mb = oracle.minibatches(oracle.Sampling(corpus, table, None, **kw))
+    assert stats[0] == n and stats[1] == (mb["ctx"] >= 0).sum() and stats[2] == len(corpus)
+    assert rel_row_error(gi, o_in) < 2e-4
+    assert rel_row_error(go, o_out) < 2e-4
+    np.testing.assert_allclose(gb[:, 1], ob[:, 1], rtol=0, atol=0)
+    np.testing.assert_allclose(gb[:, 0], ob[:, 0], rtol=1e-5)
+
+
+def test_serialised_with_subsampling_and_window_8():
+    V, D = 3000, 200
+    corpus = inputs.zipf_ids(40_000, V, 1.0, 4)
+    table, thr = oracle.build_tables(inputs.word_counts(corpus, V), 0.75, 1e-3, 10**7)
+    M_in = inputs.init_matrix(V, D, "uniform", 5)
+    M_out = inputs.init_matrix(V, D, "normal", 6, scale=0.01)
+    kw = dict(window=8, K=25, sentence_len=1000, seed=3, epoch=1, n_epochs=2)
+    o_in, o_out = M_in.copy(), M_out.copy()
+    n, _ = oracle.train_epoch(oracle.Sampling(corpus, table, thr, **kw), o_in, o_out)
+    gi, go, stats, _ = gpu_epoch(corpus, table, thr, M_in, M_out, max_inflight=1, **kw)
+    assert stats[0] == n
+    assert rel_row_error(gi, o_in) < 2e-4
+    assert rel_row_error(go, o_out) < 2e-4
+
+
+def test_untouched_rows_unchanged():
+    """Words absent from the corpus keep bitwise-identical rows."""
+    V, D = 500, 64
+    corpus = inputs.zipf_ids(20_000, 250, 1.0, 8)      # ids < 250 only
+    table, _ = oracle.build_tables(inputs.word_counts(corpus, V), 0.75, 0.0, 10**6,
+                                   want_thresh=False)
+    M_in = inputs.init_matrix(V, D, "uniform", 9)
+    M_out = inputs.init_matrix(V, D, "normal", 10, scale=0.01)
+    gi, go, _, _ = gpu_epoch(corpus, table, None, M_in, M_out, window=5, K=5,
+                             sentence_len=1000)
+    assert np.array_equal(gi[250:].view(np.uint32), M_in[250:].view(np.uint32))
+    assert np.array_equal(go[250:].view(np.uint32), M_out[250:].view(np.uint32))
+
+
+def eval_loss(M_in, M_out, t, c, n):
+    """Mean SGNS loss per input word of a fixed batch (oracle, fp64)."""
+    total, cnt = 0.0, 0
+    for b in range(len(t)):
+        A = M_in[c[b]].astype(np.float64)
+        O = M_out[np.concatenate([[t[b]], n[b]])].astype(np.float64)
+        _, _, _, loss = oracle.sgns_delta(A, O, (n[b] == t[b]).astype(np.uint8), 0.0)
+        total += loss
+        cnt += len(c[b])
+    return total / cnt
+
+
+def test_hogwild_epoch_loss_within_2_percent():
+    corpus, table, M_in, M_out = tiny_config()
+    kw = dict(window=5, K=5, sentence_len=1000, seed=7, alpha0=0.025)
+    o_in, o_out = M_in.copy(), M_out.copy()
+    oracle.train_epoch(oracle.Sampling(corpus, table, None, **kw), o_in, o_out)
+    gi, go, stats, _ = gpu_epoch(corpus, table, None, M_in, M_out, **kw)
+    # held-out evaluation minibatches from the same unigram law
+    t, c, _ = inputs.kernel_batch(2000, 6, 5, 1000, 1.0, 99)
+    n = table[np.random.default_rng(98).integers(0, len(table), (2000, 5))]
+    lo = eval_loss(o_in, o_out, t, c, n)
+    lg = eval_loss(gi, go, t, c, n)
+    l0 = eval_loss(M_in, M_out, t, c, n)
+    assert lo < 0.9 * l0                       # training moved the loss
+    assert abs(lg - lo) <= 0.02 * lo, (lg, lo, l0)
+
+
+def test_sentence_aligned_chunks_equal_one_call_when_serialised():
+    corpus, table, M_in, M_out = tiny_config(T=30_000)
+    kw = dict(window=5, K=5, sentence_len=1000, seed=2, max_inflight=1)
+    a_in, a_out, _, _ = gpu_epoch(corpus, table, None, M_in, M_out, **kw)
+    import torch
+    gi, go = to_dev(M_in), to_dev(M_out)
+    c, tb = to_dev(corpus), to_dev(table)
+    for b, e in ((0, 12_000), (12_000, 30_000)):
+        w2v.train_epoch(c, gi, go, tb, None, pos_begin=b, pos_end=e, **kw)
+    torch.cuda.synchronize()
+    assert rel_row_error(gi.cpu().numpy(), a_in.astype(np.float64)) < 1e-6
+    assert rel_row_error(go.cpu().numpy(), a_out.astype(np.float64)) < 1e-6
+
+
+def test_validation_errors():
+    import torch
+    c = torch.zeros(100, dtype=torch.int32, device="cuda")
+    M = torch.zeros((10, 8), device="cuda")
+    tb = torch.zeros(4, dtype=torch.int32, device="cuda")
+    with pytest.raises(w2v.W2VError):
+        w2v.train_epoch(c, M, M.clone(), tb, window=0)
+    with pytest.raises(w2v.W2VError):
+        w2v.train_epoch(c, M, M.clone(), tb, sentence_len=10, pos_begin=5)
+    with pytest.raises(w2v.W2VError):
+        w2v.train_epoch(c, M, M.clone(), tb, K=65)

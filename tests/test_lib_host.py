@@ -1,0 +1,121 @@
+"""Host-side checks of libw2v that need no GPU: the library loads, exports
+every entry point include/w2v.h declares, builds the same tables as the oracle
+bit for bit, and rejects invalid arguments before touching the device."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_1611_06172_amd import inputs, w2v
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_functions():
+    with open(os.path.join(ROOT, "include", "w2v.h")) as f:
+        text = f.read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(w2v_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol():
+    names = declared_functions()
+    assert len(names) >= 7
+    L = w2v.lib()
+    for name in names:
+        assert hasattr(L, name), name
+
+
+def test_version():
+    assert w2v.version() == 100
+
+
+@pytest.mark.parametrize("seed,power,t,size", [
+    (0, 0.75, 1e-4, 10**6), (1, 0.75, 0.0, 12345), (2, 1.0, 1e-2, 10**7),
+    (3, 0.5, 1e-3, 2**31 + 11)])
+def test_tables_equal_oracle(seed, power, t, size):
+    rng = np.random.default_rng(seed)
+    counts = rng.integers(0, 10**6, 3000).astype(np.int64)
+    counts[::13] = 0
+    big = size > 10**8
+    ta, ka = w2v.build_tables(counts, power, t, size, want_table=not big)
+    tb, kb = oracle.build_tables(counts, power, t, size, want_table=not big)
+    if not big:
+        assert np.array_equal(ta, tb)
+    assert np.array_equal(ka, kb)
+
+
+def test_tables_large_vocab_equal_oracle():
+    V = 1_000_000
+    counts = np.rint(inputs.zipf_pmf(V, 1.07) * 1e9).astype(np.int64)
+    ta, ka = w2v.build_tables(counts, 0.75, 1e-4, 10**8)
+    tb, kb = oracle.build_tables(counts, 0.75, 1e-4, 10**8)
+    assert np.array_equal(ta, tb) and np.array_equal(ka, kb)
+
+
+def test_table_arguments_rejected():
+    with pytest.raises(w2v.W2VError):
+        w2v.build_tables(np.array([-1, 3], np.int64))
+    with pytest.raises(w2v.W2VError):
+        w2v.build_tables(np.zeros(4, np.int64))
+    with pytest.raises(w2v.W2VError):
+        w2v.build_tables(np.ones(4, np.int64), table_size=2**32)
+    assert "table_size" in w2v.lib().w2v_last_error().decode()
+
+
+# Fake, never-dereferenced device addresses: validation must fail first.
+FAKE = 0x1000
+
+
+def train(**over):
+    args = dict(corpus=FAKE, T=1000, pos_begin=0, pos_end=1000, L=100, M_in=FAKE,
+                M_out=FAKE, V=10, D=8, ld=8, window=5, K=5, table=FAKE,
+                table_size=100, thr=None, alpha0=0.025, minf=1e-4, epoch=0,
+                n_epochs=1, seed=0, loss=None, n_b=0, stats=None, inflight=0,
+                stream=None)
+    args.update(over)
+    return w2v.lib().w2v_train_epoch(*args.values())
+
+
+@pytest.mark.parametrize("over,needle", [
+    (dict(corpus=None), "corpus"), (dict(T=0), "T"), (dict(L=0), "sentence_len"),
+    (dict(L=1025), "sentence_len"), (dict(pos_begin=50), "pos_begin"),
+    (dict(pos_end=950), "pos_end"), (dict(pos_begin=200, pos_end=100), "pos_begin"),
+    (dict(V=0), "V"), (dict(D=0), "D"), (dict(D=641, ld=641), "D"),
+    (dict(ld=7), "ld"), (dict(window=0), "window"), (dict(window=17), "window"),
+    (dict(K=-1), "K"), (dict(K=65), "K"), (dict(table_size=2**32), "table_size"),
+    (dict(table=None), "neg_table"), (dict(epoch=1), "epoch"),
+    (dict(n_epochs=0), "epoch"), (dict(M_in=None), "M_in"),
+    (dict(loss=FAKE, n_b=0), "n_buckets"), (dict(inflight=-1), "max_inflight"),
+])
+def test_train_epoch_rejects(over, needle):
+    assert train(**over) == w2v.EINVAL
+    assert needle in w2v.lib().w2v_last_error().decode()
+
+
+def step(**over):
+    args = dict(B=4, N=10, K=5, t=FAKE, c=FAKE, n=FAKE, alpha=None, a_s=0.025,
+                M_in=FAKE, M_out=FAKE, V=10, D=8, ld=8, ws=0x100000, ws_bytes=1 << 20,
+                stats=None, stream=None)
+    args.update(over)
+    return w2v.lib().w2v_step_batch(*args.values())
+
+
+@pytest.mark.parametrize("over,needle", [
+    (dict(B=-1), "B"), (dict(N=33), "N"), (dict(K=65), "K"), (dict(t=None), "targets"),
+    (dict(c=None), "contexts"), (dict(n=None), "negatives"), (dict(ws=None), "workspace"),
+    (dict(ws_bytes=100), "workspace"), (dict(ws=0x100010), "aligned"),
+    (dict(D=700, ld=700), "D"), (dict(ld=4), "ld"),
+])
+def test_step_batch_rejects(over, needle):
+    assert step(**over) == w2v.EINVAL
+    assert needle in w2v.lib().w2v_last_error().decode()
+
+
+def test_workspace_size():
+    assert w2v.step_batch_workspace_bytes(100_000, 300) == 2 * 100_000 * 300 * 8
+    assert w2v.step_batch_workspace_bytes(3, 5) == 2 * 256
+    assert w2v.step_batch_workspace_bytes(0, 5) == 0
