@@ -60,6 +60,13 @@ def main():
     ap.add_argument("--window", type=int, default=5)
     ap.add_argument("--sample", type=float, default=1e-4)
     ap.add_argument("--max-inflight", type=int, default=0)
+    ap.add_argument("--hot-tol", type=float, default=0.5,
+                    help="expected concurrent writers above which a row is "
+                         "updated atomically (w2v_hot_rows)")
+    ap.add_argument("--hot-rows", type=int, default=-1,
+                    help="override the atomic-row threshold (-1: model)")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="run a 1 GiB device copy first (counter calibration)")
     ap.add_argument("--cpu-sample-tokens", type=int, default=1_000_000)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--traffic-json",
@@ -92,6 +99,15 @@ def main():
     M_in = torch.from_numpy(M_in0).to(dev)
     M_out = torch.zeros((V, D), dtype=torch.float32, device=dev)
     stats = torch.zeros(4, dtype=torch.int64, device=dev)
+    inflight = args.max_inflight or w2v.default_inflight(D, W, K)
+    hot = (args.hot_rows if args.hot_rows >= 0 else
+           w2v.hot_rows(counts, sample_t=args.sample, window=W, K=K,
+                        inflight=inflight, tol=args.hot_tol))
+    if args.calibrate_copy:
+        src = torch.empty(1 << 28, dtype=torch.float32, device=dev)
+        src.fill_(1.0)
+        dst = src.clone()
+        del src, dst
     torch.cuda.synchronize()
     print(f"[bench] setup {time.time() - t0:.1f}s: T={T} V={V} D={D} K={K} w={W}",
           file=sys.stderr, flush=True)
@@ -102,7 +118,8 @@ def main():
         w2v.train_epoch(corpus, M_in, M_out, table, thr, window=W, K=K,
                         alpha0=0.025, min_alpha_frac=1e-4, epoch=i,
                         n_epochs=n_epochs, seed=1234, sentence_len=L,
-                        stats=stats, max_inflight=args.max_inflight)
+                        stats=stats, max_inflight=args.max_inflight,
+                        hot_rows=hot)
 
     for i in range(args.warmup):
         step(i)
@@ -155,6 +172,7 @@ def main():
                          f"T={T}, V={V}, D={D}, K={K}, window={W}, sample={args.sample}, "
                          f"sentence {L}, alpha 0.025 linear"),
             "V": V, "T": T, "D": D, "K": K, "window": W, "sample": args.sample,
+            "inflight_sentences": int(inflight), "atomic_rows": int(hot),
             "minibatches_per_step": int(n_mb), "mean_inputs_per_minibatch":
                 round(sum_n / max(n_mb, 1), 4), "retained_fraction": round(n_mb / raw, 4),
         },

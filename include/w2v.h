@@ -84,6 +84,29 @@ int w2v_build_tables(const int64_t* counts, int32_t V, double neg_power,
                      uint32_t* keep_thresh);
 
 /*
+ * Update-path choice for w2v_train_epoch (host only; no HIP call): the
+ * number H of leading ids that should receive atomic updates. With the
+ * sampling of w2v_build_tables, one minibatch writes the M_out row of word w
+ * with probability about p_out(w) = rho_w + K q_w (rho: share of w among
+ * kept words, q: its negative-sampling share) and the M_in row with
+ * probability about p_in(w) = (window + 1) rho_w. With `inflight` minibatches
+ * in flight, (inflight - 1) max(p_in, p_out) is the expected number of other
+ * minibatches writing the row while one holds it. H is one more than the
+ * largest id whose expected count reaches `tol` (0 if none), so every row at
+ * or above H is rarely written concurrently. counts as for w2v_build_tables;
+ * ids are expected to be ranked by frequency. Returns H >= 0, or a negative
+ * W2V_E* code.
+ */
+int32_t w2v_hot_rows(const int64_t* counts, int32_t V, double neg_power,
+                     double sample_t, int32_t window, int32_t K,
+                     int64_t inflight, double tol);
+
+/* Number of sentences w2v_train_epoch processes concurrently when called with
+ * max_inflight = 0 on the current device (one wavefront each), or a negative
+ * W2V_E* code. */
+int64_t w2v_default_inflight(int32_t D, int32_t window, int32_t K);
+
+/*
  * One Hogwild epoch (or a sentence-aligned part of one) of HogBatch SGD,
  * updating M_in and M_out in place on the GPU.
  *
@@ -106,11 +129,19 @@ int w2v_build_tables(const int64_t* counts, int32_t V, double neg_power,
  * input-word rows of M_in and O = [target row; negative rows] of M_out,
  *   X = A O^T, E = alpha * (l - sigma(X)), l = (1, 0, ..., 0),
  *   M_in[input words] += E O, M_out[target, negatives] += E^T A,
- * all from the rows as read at the start of the minibatch, written back with
- * fp32 atomic adds. Minibatches of one sentence run in order on one
- * wavefront; up to max_inflight sentences run concurrently and their updates
- * interleave without locks (Hogwild). max_inflight = 1 processes every
- * minibatch in sequence; 0 picks enough concurrent sentences to fill the GPU.
+ * all from the rows as read at the start of the minibatch (repeated words
+ * of one minibatch are merged, so each row is read and written once per
+ * minibatch). Minibatches of one sentence run in order on one wavefront; up
+ * to max_inflight sentences run concurrently and their updates interleave
+ * without locks (Hogwild). max_inflight = 1 processes every minibatch in
+ * sequence; 0 picks enough concurrent sentences to fill the GPU.
+ * Update path: a row with id < hot_rows receives fp32 atomic adds (no update
+ * is lost under concurrency); a row with id >= hot_rows is written back as
+ * (value read + update) with a plain store, so a concurrent update of the
+ * same row by another sentence may be overwritten, as in Hogwild. With ids
+ * ranked by frequency (id 0 the most frequent word) hot_rows selects the
+ * frequent words, whose rows see concurrent updates; hot_rows >= V makes
+ * every update atomic.
  *
  * corpus: device int32[T]. [pos_begin, pos_end) must start on a sentence
  * boundary and end on one or at T. M_in, M_out: device, see conventions.
@@ -132,7 +163,7 @@ int w2v_train_epoch(const int32_t* corpus, int64_t T, int64_t pos_begin,
                     float alpha0, float min_alpha_frac, int32_t epoch,
                     int32_t n_epochs, uint64_t seed, double* loss_buckets,
                     int32_t n_buckets, int64_t* stats, int32_t max_inflight,
-                    void* stream);
+                    int32_t hot_rows, void* stream);
 
 /*
  * The minibatches w2v_train_epoch would form over [pos_begin, pos_end),

@@ -113,6 +113,31 @@ int w2v_build_tables(const int64_t* counts, int32_t V, double neg_power,
                       keep_thresh);
 }
 
+int32_t w2v_hot_rows(const int64_t* counts, int32_t V, double neg_power,
+                     double sample_t, int32_t window, int32_t K,
+                     int64_t inflight, double tol) {
+  return hot_rows(counts, V, neg_power, sample_t, window, K, inflight, tol);
+}
+
+int64_t w2v_default_inflight(int32_t D, int32_t window, int32_t K) {
+  if (D < 1 || D > W2V_MAX_DIM)
+    return failf(W2V_EINVAL, "D must be in [1, %d]", W2V_MAX_DIM);
+  if (window < 1 || window > W2V_MAX_WINDOW)
+    return failf(W2V_EINVAL, "window must be in [1, %d]", W2V_MAX_WINDOW);
+  if (K < 0 || K > W2V_MAX_NEGATIVE)
+    return failf(W2V_EINVAL, "K must be in [0, %d]", W2V_MAX_NEGATIVE);
+  const int C = columns_for(D);
+  const int nmax = inputs_cap_for(2 * window);
+  if (C == 0 || nmax == 0 || !train_shape_supported(C, nmax))
+    return failf(W2V_EUNSUPPORTED, "no compiled kernel for D=%d window=%d", D,
+                 window);
+  const int per_cu = train_blocks_per_cu(C, nmax, K);
+  const int cus = cu_count();
+  if (per_cu <= 0 || cus <= 0) return fail(W2V_EHIP, "device query failed");
+  ok();
+  return (int64_t)per_cu * cus;
+}
+
 int w2v_train_epoch(const int32_t* corpus, int64_t T, int64_t pos_begin,
                     int64_t pos_end, int32_t sentence_len, float* M_in,
                     float* M_out, int32_t V, int32_t D, int32_t ld,
@@ -121,7 +146,7 @@ int w2v_train_epoch(const int32_t* corpus, int64_t T, int64_t pos_begin,
                     float alpha0, float min_alpha_frac, int32_t epoch,
                     int32_t n_epochs, uint64_t seed, double* loss_buckets,
                     int32_t n_buckets, int64_t* stats, int32_t max_inflight,
-                    void* stream) {
+                    int32_t hot_rows, void* stream) {
   int rc = check_sampling({corpus, T, pos_begin, pos_end, sentence_len, V,
                            window, K, neg_table, table_size, epoch, n_epochs});
   if (rc != W2V_OK) return rc;
@@ -130,6 +155,7 @@ int w2v_train_epoch(const int32_t* corpus, int64_t T, int64_t pos_begin,
   if (loss_buckets != nullptr && n_buckets < 1)
     return fail(W2V_EINVAL, "n_buckets must be >= 1 with loss_buckets");
   if (max_inflight < 0) return fail(W2V_EINVAL, "max_inflight must be >= 0");
+  if (hot_rows < 0) return fail(W2V_EINVAL, "hot_rows must be >= 0");
   const int C = columns_for(D);
   const int nmax = inputs_cap_for(2 * window);
   if (C == 0 || nmax == 0 || !train_shape_supported(C, nmax))
@@ -163,10 +189,11 @@ int w2v_train_epoch(const int32_t* corpus, int64_t T, int64_t pos_begin,
   a.loss = loss_buckets;
   a.n_buckets = n_buckets;
   a.stats = stats;
+  a.hot_rows = hot_rows;
 
   int64_t grid = max_inflight;
   if (grid == 0) {
-    const int per_cu = train_blocks_per_cu(C, nmax);
+    const int per_cu = train_blocks_per_cu(C, nmax, K);
     const int cus = cu_count();
     grid = (int64_t)(per_cu > 0 ? per_cu : 1) * (cus > 0 ? cus : 1);
   }

@@ -173,6 +173,15 @@ __device__ __forceinline__ uint64_t lanes_below(int lane) {
   return lane == 0 ? 0ull : (~0ull >> (64 - lane));
 }
 
+// Word 3 of a raw buffer descriptor (data format for untyped 32-bit access).
+constexpr int kBufferWord3 = 0x00020000;
+// Cache policy of a load that must observe agent-scope atomics of other
+// wavefronts (sc1: coherent at device scope).
+constexpr int kCoherentLoad = 16;
+
+// Cache policy of the plain (non-atomic) row stores of the Hogwild path.
+constexpr int kPlainStore = 0;
+
 // Coherent (agent-scope) row element load and fp32 atomic add; used for the
 // live matrices that other wavefronts update concurrently.
 __device__ __forceinline__ float load_live(const float* p) {

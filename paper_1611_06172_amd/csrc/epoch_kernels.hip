@@ -50,7 +50,7 @@ __device__ __forceinline__ void flush_loss(double* loss, int bucket,
   lcnt = 0.0;
 }
 
-template <int C, int NMAX, bool kExport>
+template <int C, int NMAX, bool kMulti, bool kExport>
 __global__ __launch_bounds__(kWave) void k_epoch(EpochArgs a) {
   __shared__ SentenceLds sl;
   __shared__ MinibatchLds mb;
@@ -164,17 +164,20 @@ __global__ __launch_bounds__(kWave) void k_epoch(EpochArgs a) {
         if constexpr (!kExport) {
           const int qj = q0 + j;
           const int lo = uniform_int(sl.lo[j]);
+          int ctx_id = 0;
           if (lane < n) {
             int jj = lo + lane;
             if (jj >= qj) ++jj;
-            mb.ctx[lane] = sl.ret_id[jj];
+            ctx_id = sl.ret_id[jj];
           }
+          const int n_in = stage_inputs(lane, ctx_id, lane < n, mb);
           const int neg = lane < K ? negs_lds[j * K + lane] : 0;
           const int n_out = stage_outputs(lane, sl.ret_id[qj], neg, K, mb);
           float loss_part = 0.f;
-          run_minibatch<C, NMAX, true, false>(
-              a.M_in, a.M_out, a.M_in, a.M_out, a.ld, a.D, lane, n, n_out,
-              uniform_float(sl.alpha[j]), mb, want_loss, loss_part);
+          run_minibatch<C, NMAX, kMulti, true, false>(
+              a.M_in, a.M_out, a.M_in, a.M_out, a.ld, a.D, lane, n_in, n_out,
+              uniform_float(sl.alpha[j]), a.hot_rows, mb, want_loss,
+              loss_part);
           if (want_loss) {
             const int64_t p = sb + sl.ret_off[qj];
             const int b = (int)(p * (int64_t)a.n_buckets / a.T);
@@ -207,16 +210,20 @@ __global__ __launch_bounds__(kWave) void k_epoch(EpochArgs a) {
 
 using EpochKernel = void (*)(EpochArgs);
 
-static EpochKernel train_kernel_for(int C, int nmax) {
+// Kernel for C columns per lane, up to nmax input words, and K negatives:
+// the single-block variant when the K+1 output columns fit one reduction.
+static EpochKernel train_kernel_for(int C, int nmax, int K) {
+  const bool multi = K + 1 > kWave / (nmax > 0 ? nmax : 1);
 #define W2V_PICK(c, n) \
-  if (C == c && nmax == n) return k_epoch<c, n, false>;
+  if (C == c && nmax == n) \
+    return multi ? k_epoch<c, n, true, false> : k_epoch<c, n, false, false>;
   W2V_TRAIN_SHAPES(W2V_PICK)
 #undef W2V_PICK
   return nullptr;
 }
 
 bool train_shape_supported(int C, int nmax) {
-  return train_kernel_for(C, nmax) != nullptr;
+  return train_kernel_for(C, nmax, 0) != nullptr;
 }
 
 int columns_for(int D) {
@@ -237,11 +244,11 @@ static size_t epoch_dyn_lds(const EpochArgs& a) {
   return sizeof(int32_t) * (size_t)kWave * (size_t)(a.K > 0 ? a.K : 1);
 }
 
-int train_blocks_per_cu(int C, int nmax) {
-  EpochKernel k = train_kernel_for(C, nmax);
+int train_blocks_per_cu(int C, int nmax, int K) {
+  EpochKernel k = train_kernel_for(C, nmax, K);
   if (k == nullptr) return 0;
   int blocks = 0;
-  const size_t dyn = sizeof(int32_t) * kWave * 64;
+  const size_t dyn = sizeof(int32_t) * kWave * (size_t)(K > 0 ? K : 1);
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, k, kWave, dyn) !=
       hipSuccess)
     return 0;
@@ -250,14 +257,14 @@ int train_blocks_per_cu(int C, int nmax) {
 
 hipError_t launch_train(int C, int nmax, const EpochArgs& a, int grid,
                         hipStream_t s) {
-  EpochKernel k = train_kernel_for(C, nmax);
+  EpochKernel k = train_kernel_for(C, nmax, a.K);
   if (k == nullptr) return hipErrorInvalidValue;
   hipLaunchKernelGGL(k, dim3(grid), dim3(kWave), epoch_dyn_lds(a), s, a);
   return hipGetLastError();
 }
 
 hipError_t launch_export(const EpochArgs& a, int grid, hipStream_t s) {
-  hipLaunchKernelGGL((k_epoch<1, 10, true>), dim3(grid), dim3(kWave),
+  hipLaunchKernelGGL((k_epoch<1, 10, false, true>), dim3(grid), dim3(kWave),
                      epoch_dyn_lds(a), s, a);
   return hipGetLastError();
 }

@@ -26,6 +26,7 @@ struct EpochArgs {
   double* loss;            // NULL or double[2 * n_buckets]
   int32_t n_buckets;
   int64_t* stats;          // NULL or int64[4]
+  int32_t hot_rows;        // ids below this get atomic updates
   // export outputs (minibatch export only)
   int32_t* out_targets;
   int32_t* out_ctx;
@@ -61,6 +62,6 @@ hipError_t launch_step(int C, int nmax, const StepArgs& a, int grid,
 bool train_shape_supported(int C, int nmax);
 int columns_for(int D);      // compiled C for a row length, 0 if none
 int inputs_cap_for(int n);   // compiled nmax for n input words, 0 if none
-int train_blocks_per_cu(int C, int nmax);
+int train_blocks_per_cu(int C, int nmax, int K);
 
 }  // namespace w2v

@@ -7,27 +7,33 @@
 //
 //   X = A O^T   E = alpha (l - sigma(X))   dA = E O   dO = E^T A
 //
-// Output columns are staged deduplicated: a negative equal to the target is
-// masked (weight 0) and repeated negatives collapse into one column of
-// weight m (m identical columns have identical rows, logits and errors, so
-// one column with its error scaled by m gives the same dA and dO). Every
-// output row is then read at most once per minibatch, which keeps all of a
-// minibatch's reads ahead of its own writes even when the columns are
-// processed in several blocks.
+// Rows are staged deduplicated. A negative equal to the target is masked;
+// repeated negatives collapse into one column of weight m, and repeated input
+// words into one row of weight m (m identical rows or columns have identical
+// logits and errors, so one copy with its error scaled by m yields the same
+// dA and dO). Every row is then read once and written once per minibatch:
+// all reads precede the minibatch's own writes even when the output columns
+// take several blocks, and a plain read-modify-write of a row cannot lose a
+// sibling update from the same minibatch.
 //
 // Layout: lane l holds columns l, l+64, ..., l+64(C-1) of every gathered row
-// in VGPRs (C = ceil(D/64) rounded up to a compiled size). Each (input word,
-// output word) pair leaves a per-lane partial dot product; the wave-wide
-// transposing reduction turns up to 64 such partials into one total per lane,
-// the error is evaluated lane-parallel and broadcast through LDS, and the two
-// gradient products are lane-local FMAs. Updates leave as one 64-wide
-// coalesced atomic add per row and column block: fp32 adds into the live
-// matrices (epoch training) or fp64 adds into a delta buffer (snapshot
-// batches, rounded once per element afterwards).
+// in VGPRs (C = ceil(D/64) rounded up to a compiled size), loaded through
+// range-checked buffer descriptors. Each (input word, output word) pair
+// leaves a per-lane partial dot product; the wave-wide transposing reduction
+// turns up to 64 such partials into one total per lane, the error is
+// evaluated lane-parallel and broadcast through LDS, and the two gradient
+// products are lane-local FMAs.
+//
+// Update path (live matrices): rows with id < hot_rows receive fp32 atomic
+// adds (frequent words, whose concurrent updates would otherwise overwrite
+// each other), all other rows a plain store of (value read + update), the
+// Hogwild write the paper's threads perform (Sec. 1.1). Snapshot batches add
+// their updates with fp64 atomics into a delta buffer instead.
 //
 // Output columns are processed in blocks of KB = 64 / NMAX so that one
 // block's partials fill one reduction; with K+1 <= KB (the paper's K = 5 with
-// up to ten input words) the whole minibatch is a single block.
+// up to ten input words) the whole minibatch is a single block, compiled
+// without the cross-block accumulation of the input-row updates.
 #pragma once
 
 #include "device_common.h"
@@ -39,15 +45,47 @@ constexpr int kMaxOutputs = 65;  // target + up to 64 negatives
 
 // Per-wavefront LDS staging of one minibatch's ids and its error block.
 struct MinibatchLds {
-  int ctx[kMaxInputs];      // input word ids (rows of M_in)
+  int raw_ctx[kMaxInputs];  // input words as formed
+  int ctx[kMaxInputs];      // distinct input words (rows of M_in)
+  float cwgt[kMaxInputs];   // multiplicity of each input row
   int raw[kWave];           // negatives as drawn
   int out[kMaxOutputs];     // [0] target, then distinct unmasked negatives
   float wgt[kMaxOutputs];   // multiplicity of each output column
   float E[kWave];           // error block of the current output block
 };
 
-// Stages the output columns of a minibatch; `neg` is lane k's negative for
-// k < K. Returns the number of distinct output columns (target included).
+// Stages the input rows: the lanes with `present` set hold the input words
+// in order. Returns the number of distinct input rows.
+__device__ __forceinline__ int stage_inputs(int lane, int id, bool present,
+                                            MinibatchLds& mb) {
+  const uint64_t pm = __ballot(present);
+  const int n_raw = __popcll(pm);
+  if (present) mb.raw_ctx[__popcll(pm & lanes_below(lane))] = id;
+  __syncthreads();
+  bool first = false;
+  float mult = 0.f;
+  const int mine = lane < n_raw ? mb.raw_ctx[lane] : -1;
+  if (lane < n_raw) {
+    first = true;
+    for (int i = 0; i < n_raw; ++i) {
+      if (mb.raw_ctx[i] == mine) {
+        if (i < lane) first = false;
+        mult += 1.f;
+      }
+    }
+  }
+  const uint64_t m = __ballot(first);
+  if (first) {
+    const int dst = __popcll(m & lanes_below(lane));
+    mb.ctx[dst] = mine;
+    mb.cwgt[dst] = mult;
+  }
+  __syncthreads();
+  return __popcll(m);
+}
+
+// Stages the output columns; `neg` is lane k's negative for k < K.
+// Returns the number of distinct output columns (target included).
 __device__ __forceinline__ int stage_outputs(int lane, int target, int neg,
                                              int K, MinibatchLds& mb) {
   if (lane < K) mb.raw[lane] = neg;
@@ -57,8 +95,7 @@ __device__ __forceinline__ int stage_outputs(int lane, int target, int neg,
   if (lane < K && neg != target) {
     first = true;
     for (int k = 0; k < K; ++k) {
-      const int other = mb.raw[k];
-      if (other == neg) {
+      if (mb.raw[k] == neg) {
         if (k < lane) first = false;
         mult += 1.f;
       }
@@ -78,21 +115,54 @@ __device__ __forceinline__ int stage_outputs(int lane, int target, int neg,
   return 1 + __popcll(m);
 }
 
-template <bool kLive>
-__device__ __forceinline__ float load_row_elem(const float* p) {
-  if constexpr (kLive) {
-    return load_live(p);
-  } else {
-    return *p;
-  }
+// Raw buffer descriptor of one matrix row of n_bytes: loads past the end
+// return 0 and stores/atomics past it are dropped by the hardware range
+// check, so a row of D floats needs no per-lane bounds test.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t row_rsrc(const void* row,
+                                                          int n_bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(row), (short)0,
+                                           n_bytes, kBufferWord3);
 }
 
-template <bool kAccum64>
-__device__ __forceinline__ void add_update(void* base, int64_t off, float g) {
+// Loads columns lane + 64c, c < C, of one row (0 past D).
+template <int C, bool kLive>
+__device__ __forceinline__ void load_row(const float* base, int64_t id,
+                                         int64_t ld, int D, int lane,
+                                         float (&r)[C]) {
+  const __amdgpu_buffer_rsrc_t rs = row_rsrc(base + id * ld, D * 4);
+#pragma unroll
+  for (int c = 0; c < C; ++c)
+    r[c] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
+        rs, (lane + kWave * c) * 4, 0, kLive ? kCoherentLoad : 0));
+}
+
+// Applies update g to one row whose values as read are `old`: fp64 atomics
+// into a delta buffer (kAccum64), fp32 atomics for hot rows, otherwise a
+// plain store of old + g.
+template <int C, bool kAccum64>
+__device__ __forceinline__ void update_row(void* base, int64_t id, int64_t ld,
+                                           int D, int lane, int hot_rows,
+                                           const float (&old)[C],
+                                           const float (&g)[C]) {
   if constexpr (kAccum64) {
-    unsafeAtomicAdd((double*)base + off, (double)g);
+    double* row = (double*)base + id * ld;
+#pragma unroll
+    for (int c = 0; c < C; ++c)
+      if (lane + kWave * c < D) unsafeAtomicAdd(row + lane + kWave * c, (double)g[c]);
   } else {
-    add_live((float*)base + off, g);
+    const __amdgpu_buffer_rsrc_t rs = row_rsrc((float*)base + id * ld, D * 4);
+    if (id < hot_rows) {
+#pragma unroll
+      for (int c = 0; c < C; ++c)
+        __builtin_amdgcn_raw_ptr_buffer_atomic_fadd_f32(
+            g[c], rs, (lane + kWave * c) * 4, 0, 0);
+    } else {
+#pragma unroll
+      for (int c = 0; c < C; ++c)
+        __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(old[c] + g[c]), rs,
+                                              (lane + kWave * c) * 4, 0,
+                                              kPlainStore);
+    }
   }
 }
 
@@ -102,76 +172,79 @@ __device__ __forceinline__ float softplus(float z) {
 }
 
 // Runs one minibatch. Rin/Rout: where rows are read; Win/Wout: where updates
-// are added (fp32 matrices, or fp64 delta buffers with the same row stride
-// when kAccum64). n input words (n <= NMAX) in mb.ctx, n_out staged output
-// columns in mb.out/mb.wgt. Every lane returns its share of the minibatch
-// loss in `loss_part` when want_loss is set.
-template <int C, int NMAX, bool kLiveRead, bool kAccum64>
+// go (the same fp32 matrices, or fp64 delta buffers with the same row stride
+// when kAccum64). n distinct input rows (n <= NMAX) in mb.ctx/mb.cwgt, n_out
+// distinct output columns in mb.out/mb.wgt. Every lane returns its share of
+// the minibatch loss in `loss_part` when want_loss is set.
+template <int C, int NMAX, bool kMulti, bool kLiveRead, bool kAccum64>
 __device__ __forceinline__ void run_minibatch(
     const float* Rin, const float* Rout, void* Win, void* Wout, int64_t ld,
-    int D, int lane, int n, int n_out, float alpha, MinibatchLds& mb,
-    bool want_loss, float& loss_part) {
+    int D, int lane, int n, int n_out, float alpha, int hot_rows,
+    MinibatchLds& mb, bool want_loss, float& loss_part) {
   constexpr int KB = kWave / NMAX;
-  static_assert(KB >= 1, "NMAX must be <= 64");
-  bool ok[C];
-#pragma unroll
-  for (int c = 0; c < C; ++c) ok[c] = lane + kWave * c < D;
+  constexpr int kSlots = NMAX * KB;
+  static_assert(KB >= 1 && kSlots <= kWave, "NMAX must be <= 64");
 
-  // Gather the input-word rows once.
+  // Gather the input-word rows once (rows >= n stay zero).
   float a[NMAX][C];
 #pragma unroll
   for (int i = 0; i < NMAX; ++i) {
     if (i < n) {
-      const int id = uniform_int(mb.ctx[i]);
-      const float* row = Rin + (int64_t)id * ld + lane;
-#pragma unroll
-      for (int c = 0; c < C; ++c)
-        a[i][c] = ok[c] ? load_row_elem<kLiveRead>(row + kWave * c) : 0.f;
+      load_row<C, kLiveRead>(Rin, uniform_int(mb.ctx[i]), ld, D, lane, a[i]);
     } else {
 #pragma unroll
       for (int c = 0; c < C; ++c) a[i][c] = 0.f;
     }
   }
+  // Input-row updates accumulate over output blocks (kMulti); with a single
+  // block (n_out <= KB guaranteed by the caller) they are applied directly.
+  float ga[kMulti ? NMAX : 1][C];
+  if constexpr (kMulti) {
+#pragma unroll
+    for (int i = 0; i < NMAX; ++i)
+#pragma unroll
+      for (int c = 0; c < C; ++c) ga[i][c] = 0.f;
+  }
 
-  for (int k0 = 0; k0 < n_out; k0 += KB) {
+  for (int k0 = 0; k0 < (kMulti ? n_out : 1); k0 += KB) {
     float o[KB][C];
 #pragma unroll
     for (int kk = 0; kk < KB; ++kk) {
       if (k0 + kk < n_out) {
-        const int id = uniform_int(mb.out[k0 + kk]);
-        const float* row = Rout + (int64_t)id * ld + lane;
-#pragma unroll
-        for (int c = 0; c < C; ++c)
-          o[kk][c] = ok[c] ? load_row_elem<kLiveRead>(row + kWave * c) : 0.f;
+        load_row<C, kLiveRead>(Rout, uniform_int(mb.out[k0 + kk]), ld, D, lane,
+                               o[kk]);
       } else {
 #pragma unroll
         for (int c = 0; c < C; ++c) o[kk][c] = 0.f;
       }
     }
 
-    // Per-lane partial logits of the block, slot i*KB + kk.
+    // Per-lane partial logits, slot s = i*KB + kk.
     float v[kWave];
 #pragma unroll
     for (int i = 0; i < NMAX; ++i) {
+      if (i < n) {
 #pragma unroll
-      for (int kk = 0; kk < KB; ++kk) {
-        float acc = 0.f;
-        if (i < n) {
+        for (int kk = 0; kk < KB; ++kk) {
+          float acc = 0.f;
 #pragma unroll
           for (int c = 0; c < C; ++c) acc = fmaf(a[i][c], o[kk][c], acc);
+          v[i * KB + kk] = acc;
         }
-        v[i * KB + kk] = acc;
+      } else {
+#pragma unroll
+        for (int kk = 0; kk < KB; ++kk) v[i * KB + kk] = 0.f;
       }
     }
 #pragma unroll
-    for (int s = NMAX * KB; s < kWave; ++s) v[s] = 0.f;
+    for (int s = kSlots; s < kWave; ++s) v[s] = 0.f;
     const float x = xpose_reduce64(v, lane);
 
-    // Error of slot `lane` (input li, output column lk).
+    // Error of slot `lane` (input row li, output column lk).
     const int li = lane / KB;
     const int lk = k0 + lane % KB;
-    const bool valid = lane < NMAX * KB && li < n && lk < n_out;
-    const float wgt = valid ? mb.wgt[lk] : 0.f;
+    const bool valid = lane < kSlots && li < n && lk < n_out;
+    const float wgt = valid ? mb.wgt[lk] * mb.cwgt[li] : 0.f;
     // label - sigma(x) is sigma(-x) for the target and -sigma(x) for a
     // negative; evaluating sigma(z) directly avoids cancelling against 1.
     const float z = (lk == 0) ? -x : x;
@@ -196,33 +269,41 @@ __device__ __forceinline__ void run_minibatch(
             for (int c = 0; c < C; ++c) g[c] = fmaf(e, a[i][c], g[c]);
           }
         }
-        const int64_t off = (int64_t)uniform_int(mb.out[k]) * ld + lane;
-#pragma unroll
-        for (int c = 0; c < C; ++c)
-          if (ok[c]) add_update<kAccum64>(Wout, off + kWave * c, g[c]);
+        update_row<C, kAccum64>(Wout, uniform_int(mb.out[k]), ld, D, lane,
+                                hot_rows, o[kk], g);
       }
     }
 
-    // dA = E O for every input row (per block when there are several).
+    // dA = E O (accumulated over output blocks when there are several).
 #pragma unroll
     for (int i = 0; i < NMAX; ++i) {
       if (i < n) {
         float g[C];
 #pragma unroll
-        for (int c = 0; c < C; ++c) g[c] = 0.f;
+        for (int c = 0; c < C; ++c) g[c] = kMulti ? ga[kMulti ? i : 0][c] : 0.f;
 #pragma unroll
         for (int kk = 0; kk < KB; ++kk) {
           const float e = mb.E[i * KB + kk];
 #pragma unroll
           for (int c = 0; c < C; ++c) g[c] = fmaf(e, o[kk][c], g[c]);
         }
-        const int64_t off = (int64_t)uniform_int(mb.ctx[i]) * ld + lane;
+        if constexpr (kMulti) {
 #pragma unroll
-        for (int c = 0; c < C; ++c)
-          if (ok[c]) add_update<kAccum64>(Win, off + kWave * c, g[c]);
+          for (int c = 0; c < C; ++c) ga[i][c] = g[c];
+        } else {
+          update_row<C, kAccum64>(Win, uniform_int(mb.ctx[i]), ld, D, lane,
+                                  hot_rows, a[i], g);
+        }
       }
     }
     __syncthreads();
+  }
+  if constexpr (kMulti) {
+#pragma unroll
+    for (int i = 0; i < NMAX; ++i)
+      if (i < n)
+        update_row<C, kAccum64>(Win, uniform_int(mb.ctx[i]), ld, D, lane,
+                                hot_rows, a[i], ga[i]);
   }
 }
 

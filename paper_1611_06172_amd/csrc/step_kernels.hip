@@ -20,7 +20,7 @@ __global__ __launch_bounds__(256) void k_zero(double* p, int64_t n) {
     p[i] = 0.0;
 }
 
-template <int C, int NMAX>
+template <int C, int NMAX, bool kMulti>
 __global__ __launch_bounds__(kWave) void k_step(StepArgs a) {
   __shared__ MinibatchLds mb;
   const int lane = threadIdx.x;
@@ -33,9 +33,8 @@ __global__ __launch_bounds__(kWave) void k_step(StepArgs a) {
     if (lane < a.N) c = a.contexts[b * a.N + lane];
     bad |= (c < -1 || c >= a.V);
     const bool present = c >= 0;
-    const uint64_t m = __ballot(present);
-    if (present) mb.ctx[__popcll(m & lanes_below(lane))] = c;
-    const int n = __popcll(m);
+    const int n = __popcll(__ballot(present));
+    const int n_in = stage_inputs(lane, c, present, mb);
     int neg = 0;
     if (lane < a.K) {
       neg = a.negatives[b * a.K + lane];
@@ -50,9 +49,9 @@ __global__ __launch_bounds__(kWave) void k_step(StepArgs a) {
       sum_n += n;
       const float alpha = a.alpha != nullptr ? a.alpha[b] : a.alpha_scalar;
       float unused = 0.f;
-      run_minibatch<C, NMAX, false, true>(a.M_in, a.M_out, a.dM_in, a.dM_out,
-                                          a.ld, a.D, lane, n, n_out, alpha, mb,
-                                          false, unused);
+      run_minibatch<C, NMAX, kMulti, false, true>(a.M_in, a.M_out, a.dM_in, a.dM_out,
+                                          a.ld, a.D, lane, n_in, n_out, alpha,
+                                          0, mb, false, unused);
     }
     __syncthreads();
   }
@@ -84,9 +83,10 @@ __global__ __launch_bounds__(256) void k_finalize(float* M, const double* dM,
 
 using StepKernel = void (*)(StepArgs);
 
-static StepKernel step_kernel_for(int C, int nmax) {
+static StepKernel step_kernel_for(int C, int nmax, int K) {
+  const bool multi = K + 1 > kWave / nmax;
 #define W2V_PICK(c, n) \
-  if (C == c && nmax == n) return k_step<c, n>;
+  if (C == c && nmax == n) return multi ? k_step<c, n, true> : k_step<c, n, false>;
   W2V_STEP_SHAPES(W2V_PICK)
 #undef W2V_PICK
   return nullptr;
@@ -94,7 +94,7 @@ static StepKernel step_kernel_for(int C, int nmax) {
 
 hipError_t launch_step(int C, int nmax, const StepArgs& a, int grid,
                        hipStream_t s) {
-  StepKernel k = step_kernel_for(C, nmax);
+  StepKernel k = step_kernel_for(C, nmax, a.K);
   if (k == nullptr) return hipErrorInvalidValue;
   const int64_t n_delta = (int64_t)a.V * a.ld;
   hipLaunchKernelGGL(k_zero, dim3(4096), dim3(256), 0, s, a.dM_in, n_delta);

@@ -74,4 +74,48 @@ int build_tables(const int64_t* counts, int32_t V, double power,
   return ok();
 }
 
+int hot_rows(const int64_t* counts, int32_t V, double power, double sample_t,
+             int32_t window, int32_t K, int64_t inflight, double tol) {
+  if (counts == nullptr) return fail(W2V_EINVAL, "counts is NULL");
+  if (V <= 0) return fail(W2V_EINVAL, "V must be positive");
+  if (window < 1 || K < 0) return fail(W2V_EINVAL, "need window >= 1, K >= 0");
+  if (inflight < 1) return fail(W2V_EINVAL, "inflight must be >= 1");
+  if (!(tol > 0.0)) return fail(W2V_EINVAL, "tol must be positive");
+  if (!(sample_t >= 0.0)) return fail(W2V_EINVAL, "sample_t must be >= 0");
+  int64_t total = 0;
+  for (int32_t w = 0; w < V; ++w) {
+    if (counts[w] < 0) return fail(W2V_EINVAL, "negative count");
+    total += counts[w];
+  }
+  if (total <= 0) return fail(W2V_EINVAL, "counts sum to zero");
+  // Kept mass per word and negative-sampling weight per word.
+  double kept_sum = 0.0, neg_sum = 0.0;
+  std::vector<double> kept((size_t)V), negw((size_t)V);
+  for (int32_t w = 0; w < V; ++w) {
+    const double c = (double)counts[w];
+    double p = 1.0;
+    if (sample_t > 0.0 && counts[w] > 0) {
+      const double r = sample_t / (c / (double)total);
+      p = sqrt(r) + r;
+      if (p > 1.0) p = 1.0;
+    }
+    kept[(size_t)w] = c * p;
+    negw[(size_t)w] = pow(c, power);
+    kept_sum += kept[(size_t)w];
+    neg_sum += negw[(size_t)w];
+  }
+  const double others = (double)(inflight - 1);
+  int32_t H = 0;
+  for (int32_t w = 0; w < V; ++w) {
+    const double rho = kept[(size_t)w] / kept_sum;
+    const double q = negw[(size_t)w] / neg_sum;
+    const double p_out = rho + (double)K * q;
+    const double p_in = (double)(window + 1) * rho;
+    const double p = p_out > p_in ? p_out : p_in;
+    if (others * p >= tol) H = w + 1;
+  }
+  ok();
+  return H;
+}
+
 }  // namespace w2v

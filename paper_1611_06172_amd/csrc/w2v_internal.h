@@ -3,7 +3,7 @@
 
 #include <stdint.h>
 
-#include "../../include/w2v.h"
+#include "w2v.h"
 
 namespace w2v {
 
@@ -13,6 +13,9 @@ int fail(int code, const char* msg);
 int failf(int code, const char* fmt, ...);
 // Clears this thread's last error and returns W2V_OK.
 int ok();
+
+int hot_rows(const int64_t* counts, int32_t V, double power, double sample_t,
+             int32_t window, int32_t K, int64_t inflight, double tol);
 
 int build_tables(const int64_t* counts, int32_t V, double power,
                  double sample_t, int32_t* table, int64_t table_size,

@@ -55,12 +55,17 @@ def lib():
     L.w2v_build_tables.restype = ctypes.c_int
     L.w2v_train_epoch.argtypes = [
         _vp, _i64, _i64, _i64, _i32, _vp, _vp, _i32, _i32, _i32, _i32, _i32,
-        _vp, _i64, _vp, _f32, _f32, _i32, _i32, _u64, _vp, _i32, _vp, _i32, _vp]
+        _vp, _i64, _vp, _f32, _f32, _i32, _i32, _u64, _vp, _i32, _vp, _i32, _i32,
+        _vp]
     L.w2v_train_epoch.restype = ctypes.c_int
     L.w2v_debug_minibatches.argtypes = [
         _vp, _i64, _i64, _i64, _i32, _i32, _i32, _i32, _vp, _i64, _vp, _f32,
         _f32, _i32, _i32, _u64, _vp, _vp, _vp, _vp, _vp, _vp, _vp]
     L.w2v_debug_minibatches.restype = ctypes.c_int
+    L.w2v_hot_rows.argtypes = [_vp, _i32, _f64, _f64, _i32, _i32, _i64, _f64]
+    L.w2v_hot_rows.restype = ctypes.c_int32
+    L.w2v_default_inflight.argtypes = [_i32, _i32, _i32]
+    L.w2v_default_inflight.restype = ctypes.c_int64
     L.w2v_step_batch_workspace_bytes.argtypes = [_i32, _i32]
     L.w2v_step_batch_workspace_bytes.restype = ctypes.c_size_t
     L.w2v_step_batch.argtypes = [
@@ -131,14 +136,38 @@ def build_tables(counts, neg_power: float = 0.75, sample_t: float = 1e-4,
     return table, thr
 
 
+def hot_rows(counts, *, neg_power: float = 0.75, sample_t: float = 1e-4,
+             window: int = 5, K: int = 5, inflight: int, tol: float = 0.5) -> int:
+    """Leading ids to update atomically (see w2v_hot_rows)."""
+    counts = np.ascontiguousarray(counts, dtype=np.int64)
+    h = int(lib().w2v_hot_rows(counts.ctypes.data, counts.shape[0],
+                                float(neg_power), float(sample_t), window, K,
+                                int(inflight), float(tol)))
+    if h < 0:
+        _check(h)
+    return h
+
+
+def default_inflight(D: int, window: int = 5, K: int = 5) -> int:
+    """Concurrent sentences of train_epoch with max_inflight = 0."""
+    n = int(lib().w2v_default_inflight(D, window, K))
+    if n < 0:
+        _check(n)
+    return n
+
+
 def train_epoch(corpus, M_in, M_out, neg_table, keep_thresh=None, *,
                 window: int = 5, K: int = 5, D: Optional[int] = None,
                 alpha0: float = 0.025, min_alpha_frac: float = 1e-4,
                 epoch: int = 0, n_epochs: int = 1, seed: int = 0,
                 pos_begin: int = 0, pos_end: Optional[int] = None,
                 sentence_len: int = 1000, loss_buckets=None, stats=None,
-                max_inflight: int = 0, stream=None):
-    """Hogwild HogBatch epoch over corpus[pos_begin:pos_end], in place."""
+                max_inflight: int = 0, hot_rows: Optional[int] = None,
+                stream=None):
+    """Hogwild HogBatch epoch over corpus[pos_begin:pos_end], in place.
+
+    hot_rows: ids below it are updated with atomic adds, the others with
+    plain read-modify-write stores; None makes every update atomic."""
     import torch
     _dev(corpus, torch.int32, "corpus", 1)
     V, ld = _matrix(M_in, "M_in")
@@ -163,7 +192,8 @@ def train_epoch(corpus, M_in, M_out, neg_table, keep_thresh=None, *,
         _ptr(corpus), T, pos_begin, end, sentence_len, _ptr(M_in), _ptr(M_out),
         V, D, ld, window, K, _ptr(neg_table), neg_table.numel(),
         _ptr(keep_thresh), alpha0, min_alpha_frac, epoch, n_epochs, seed,
-        _ptr(loss_buckets), n_b, _ptr(stats), max_inflight, _stream(stream)))
+        _ptr(loss_buckets), n_b, _ptr(stats), max_inflight,
+        V if hot_rows is None else int(hot_rows), _stream(stream)))
 
 
 def debug_minibatches(corpus, neg_table, keep_thresh=None, *, V: int,

@@ -79,6 +79,20 @@ def test_serialised_with_subsampling_and_window_8():
     assert rel_row_error(go, o_out) < 2e-4
 
 
+@pytest.mark.parametrize("hot", [0, 37])
+def test_serialised_plain_and_mixed_update_paths(hot):
+    """Plain read-modify-write stores (ids >= hot) give the same serialised
+    result as atomics: within one wavefront nothing races."""
+    corpus, table, M_in, M_out = tiny_config(T=30_000)
+    kw = dict(window=5, K=5, sentence_len=1000, seed=11)
+    o_in, o_out = M_in.copy(), M_out.copy()
+    oracle.train_epoch(oracle.Sampling(corpus, table, None, **kw), o_in, o_out)
+    gi, go, _, _ = gpu_epoch(corpus, table, None, M_in, M_out, max_inflight=1,
+                             hot_rows=hot, **kw)
+    assert rel_row_error(gi, o_in) < 2e-4
+    assert rel_row_error(go, o_out) < 2e-4
+
+
 def test_untouched_rows_unchanged():
     """Words absent from the corpus keep bitwise-identical rows."""
     V, D = 500, 64
@@ -105,12 +119,18 @@ def eval_loss(M_in, M_out, t, c, n):
     return total / cnt
 
 
-def test_hogwild_epoch_loss_within_2_percent():
+@pytest.mark.parametrize("update_path", ["atomic", "model"])
+def test_hogwild_epoch_loss_within_2_percent(update_path):
     corpus, table, M_in, M_out = tiny_config()
     kw = dict(window=5, K=5, sentence_len=1000, seed=7, alpha0=0.025)
     o_in, o_out = M_in.copy(), M_out.copy()
     oracle.train_epoch(oracle.Sampling(corpus, table, None, **kw), o_in, o_out)
-    gi, go, stats, _ = gpu_epoch(corpus, table, None, M_in, M_out, **kw)
+    hot = None
+    if update_path == "model":
+        counts = inputs.word_counts(corpus, 1000)
+        hot = w2v.hot_rows(counts, sample_t=0.0, inflight=200, tol=0.5)
+        assert 0 < hot < 1000
+    gi, go, stats, _ = gpu_epoch(corpus, table, None, M_in, M_out, hot_rows=hot, **kw)
     # held-out evaluation minibatches from the same unigram law
     t, c, _ = inputs.kernel_batch(2000, 6, 5, 1000, 1.0, 99)
     n = table[np.random.default_rng(98).integers(0, len(table), (2000, 5))]

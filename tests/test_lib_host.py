@@ -75,7 +75,7 @@ def train(**over):
                 M_out=FAKE, V=10, D=8, ld=8, window=5, K=5, table=FAKE,
                 table_size=100, thr=None, alpha0=0.025, minf=1e-4, epoch=0,
                 n_epochs=1, seed=0, loss=None, n_b=0, stats=None, inflight=0,
-                stream=None)
+                hot=0, stream=None)
     args.update(over)
     return w2v.lib().w2v_train_epoch(*args.values())
 
@@ -90,6 +90,7 @@ def train(**over):
     (dict(table=None), "neg_table"), (dict(epoch=1), "epoch"),
     (dict(n_epochs=0), "epoch"), (dict(M_in=None), "M_in"),
     (dict(loss=FAKE, n_b=0), "n_buckets"), (dict(inflight=-1), "max_inflight"),
+    (dict(hot=-1), "hot_rows"),
 ])
 def test_train_epoch_rejects(over, needle):
     assert train(**over) == w2v.EINVAL
@@ -119,3 +120,27 @@ def test_workspace_size():
     assert w2v.step_batch_workspace_bytes(100_000, 300) == 2 * 100_000 * 300 * 8
     assert w2v.step_batch_workspace_bytes(3, 5) == 2 * 256
     assert w2v.step_batch_workspace_bytes(0, 5) == 0
+
+
+def test_hot_rows_model():
+    """Uniform counts: every word has the same write rate, so either all rows
+    or none are hot; the count grows with the number in flight."""
+    V = 1000
+    counts = np.full(V, 10, np.int64)
+    # rho = 1/V, q = 1/V -> p = max(rho + K q, (w+1) rho) = 6/V with K=5, w=5
+    p = 6.0 / V
+    assert w2v.hot_rows(counts, sample_t=0.0, inflight=int(0.5 / p) + 2, tol=0.5) == V
+    assert w2v.hot_rows(counts, sample_t=0.0, inflight=int(0.5 / p) - 1, tol=0.5) == 0
+    zipf = np.rint(inputs.zipf_pmf(100_000, 1.07) * 1e8).astype(np.int64)
+    hs = [w2v.hot_rows(zipf, inflight=f) for f in (16, 256, 4096)]
+    assert hs[0] < hs[1] < hs[2] < 100_000
+    assert w2v.hot_rows(zipf, inflight=256, tol=0.1) > hs[1]
+
+
+def test_hot_rows_rejects():
+    c = np.ones(4, np.int64)
+    for kw in (dict(inflight=0), dict(tol=0.0), dict(window=0), dict(K=-1)):
+        args = dict(inflight=10)
+        args.update(kw)
+        with pytest.raises(w2v.W2VError):
+            w2v.hot_rows(c, **args)
