@@ -24,7 +24,7 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0   # MI355X HBM3E, 8 TB/s
 METRIC = "Mwords/sec at V=1M D=300 K=5 window=5 (1 GPU); achieved HBM GB/s"
 KERNEL_SOURCES = ["device_common.h", "sgns_core.h", "kernel_args.h",
-                  "epoch_kernels.hip"]
+                  "sentence.h", "epoch_kernels.hip", "epoch_pipe.hip"]
 
 
 def kernel_hash():

@@ -135,6 +135,16 @@ int64_t w2v_default_inflight(int32_t D, int32_t window, int32_t K);
  * to max_inflight sentences run concurrently and their updates interleave
  * without locks (Hogwild). max_inflight = 1 processes every minibatch in
  * sequence; 0 picks enough concurrent sentences to fill the GPU.
+ * Two kernels implement this. The default loads and writes every row per
+ * minibatch. An experimental pipelined kernel, selected by the environment
+ * variable W2V_EPOCH_KERNEL=pipe where the K+1 output words fit one
+ * reduction block (K + 1 <= 64 / (2 window) rounded to the compiled input
+ * capacity), keeps each sentence's window of input rows in LDS, prefetches
+ * one minibatch ahead and writes an input row of a word with id >= hot_rows
+ * back once, when it leaves the window (its updates are summed there
+ * first). Both keep the per-sentence order exact; the pipelined kernel
+ * holds rare input rows longer, so more concurrent updates to them are
+ * overwritten.
  * Update path: a row with id < hot_rows receives fp32 atomic adds (no update
  * is lost under concurrency); a row with id >= hot_rows is written back as
  * (value read + update) with a plain store, so a concurrent update of the

@@ -3,6 +3,7 @@
 // call, so a rejected call has no device side effect.
 #include <stdarg.h>
 #include <stdio.h>
+#include <stdlib.h>
 #include <string.h>
 
 #include <mutex>
@@ -96,6 +97,19 @@ static int check_matrices(const float* M_in, const float* M_out, int32_t V,
   return W2V_OK;
 }
 
+// Epoch kernel choice: the general kernel, or the pipelined one where it
+// applies when the environment variable W2V_EPOCH_KERNEL is "pipe".
+static bool use_pipe(int C, int nmax, int K) {
+  const char* v = getenv("W2V_EPOCH_KERNEL");
+  if (v == nullptr || strcmp(v, "pipe") != 0) return false;
+  return pipe_applies(C, nmax, K);
+}
+
+static int epoch_blocks_per_cu(int C, int nmax, int window, int K) {
+  return use_pipe(C, nmax, K) ? pipe_blocks_per_cu(C, nmax, window, K)
+                              : train_blocks_per_cu(C, nmax, K);
+}
+
 }  // namespace w2v
 
 using namespace w2v;
@@ -131,7 +145,7 @@ int64_t w2v_default_inflight(int32_t D, int32_t window, int32_t K) {
   if (C == 0 || nmax == 0 || !train_shape_supported(C, nmax))
     return failf(W2V_EUNSUPPORTED, "no compiled kernel for D=%d window=%d", D,
                  window);
-  const int per_cu = train_blocks_per_cu(C, nmax, K);
+  const int per_cu = epoch_blocks_per_cu(C, nmax, window, K);
   const int cus = cu_count();
   if (per_cu <= 0 || cus <= 0) return fail(W2V_EHIP, "device query failed");
   ok();
@@ -193,13 +207,15 @@ int w2v_train_epoch(const int32_t* corpus, int64_t T, int64_t pos_begin,
 
   int64_t grid = max_inflight;
   if (grid == 0) {
-    const int per_cu = train_blocks_per_cu(C, nmax, K);
+    const int per_cu = epoch_blocks_per_cu(C, nmax, window, K);
     const int cus = cu_count();
     grid = (int64_t)(per_cu > 0 ? per_cu : 1) * (cus > 0 ? cus : 1);
   }
   if (grid > n_sent) grid = n_sent;
   if (grid > (1 << 30)) grid = 1 << 30;
-  hipError_t e = launch_train(C, nmax, a, (int)grid, (hipStream_t)stream);
+  hipError_t e = use_pipe(C, nmax, K)
+                     ? launch_pipe(C, nmax, a, (int)grid, (hipStream_t)stream)
+                     : launch_train(C, nmax, a, (int)grid, (hipStream_t)stream);
   if (e != hipSuccess) return hip_fail(e, "train kernel launch");
   return ok();
 }

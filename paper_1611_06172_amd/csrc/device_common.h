@@ -161,6 +161,23 @@ __device__ __forceinline__ float wave_sum(float x) {
   return x;
 }
 
+// Orders LDS accesses between the lanes of a single-wavefront workgroup.
+// The LDS executes one wavefront's instructions in issue order, so the only
+// thing to prevent is the compiler moving LDS accesses across this point; a
+// workgroup barrier would also make the wavefront wait for all of its
+// outstanding global loads and stores.
+__device__ __forceinline__ void wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// Waits until every global load, store and atomic of this wavefront has
+// completed (s_waitcnt vmcnt(0); expcnt and lgkmcnt left unconstrained).
+__device__ __forceinline__ void wait_global() {
+  __builtin_amdgcn_s_waitcnt(0x0F70);
+}
+
 __device__ __forceinline__ int uniform_int(int x) {
   return __builtin_amdgcn_readfirstlane(x);
 }

@@ -1,64 +1,31 @@
-// Sentence-parallel HogBatch epoch on gfx950.
+// Sentence-parallel HogBatch epoch on gfx950: the general kernel.
 //
 // One wavefront owns one sentence at a time (a persistent grid strides over
 // the sentences of the range). For its sentence it
-//   1. reads the raw ids, decides subsampling per position (Philox word 0
-//      against the keep threshold) and compacts the kept words into LDS with a
-//      ballot prefix count;
-//   2. forms 64 targets at a time lane-parallel: window half-width (word 1),
-//      the K shared negatives (words 2.., one table read each) and the
-//      decayed learning rate;
+//   1. decides subsampling and compacts the kept words (sentence.h);
+//   2. forms 64 targets at a time lane-parallel (sentence.h);
 //   3. runs those targets' minibatches in sentence order through the fused
 //      minibatch (sgns_core.h), so every minibatch of a sentence sees the
 //      updates of the ones before it, while minibatches of different
 //      sentences interleave without locks (Hogwild, Sec. 1.1).
-// The export variant stops after step 2 and writes the minibatches out.
+// It serves every compiled shape, including output blocks that take several
+// reductions; the pipelined kernel (epoch_pipe.hip) serves the single-block
+// shapes. The export variant stops after step 2 and writes the minibatches
+// out.
 #include "kernel_args.h"
+#include "sentence.h"
 #include "sgns_core.h"
 
 namespace w2v {
 
-constexpr int kMaxSentence = 1024;
-
-struct SentenceLds {
-  int32_t ret_id[kMaxSentence];   // kept word ids, in order
-  int16_t ret_off[kMaxSentence];  // their offsets in the sentence
-  int32_t lo[kWave];              // first retained index of the window
-  int32_t n[kWave];               // number of input words
-  float alpha[kWave];
-  uint64_t mask[kWave];           // bit k: negative k equals the target
-  int32_t bad[kWave];             // a negative id outside [0, V)
-};
-
-__device__ __forceinline__ uint32_t word_of(const U64x4& b, int j) {
-  const int m = j >> 1;
-  const uint64_t v = m == 0 ? b.v[0] : m == 1 ? b.v[1] : m == 2 ? b.v[2] : b.v[3];
-  return (j & 1) ? (uint32_t)(v >> 32) : (uint32_t)v;
-}
-
-__device__ __forceinline__ void flush_loss(double* loss, int bucket,
-                                           double& lsum, double& lcnt,
-                                           int lane) {
-  double s = lsum;
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) s += __shfl_xor(s, m);
-  if (lane == 0) {
-    unsafeAtomicAdd(loss + 2 * bucket, s);
-    unsafeAtomicAdd(loss + 2 * bucket + 1, lcnt);
-  }
-  lsum = 0.0;
-  lcnt = 0.0;
-}
-
 template <int C, int NMAX, bool kMulti, bool kExport>
 __global__ __launch_bounds__(kWave) void k_epoch(EpochArgs a) {
   __shared__ SentenceLds sl;
+  __shared__ TargetBatch tb;
   __shared__ MinibatchLds mb;
   extern __shared__ int32_t negs_lds[];  // [kWave][K]
   const int lane = threadIdx.x;
-  const uint64_t e = (uint64_t)a.epoch;
   const int K = a.K;
-  const int w = a.w;
   const bool want_loss = a.loss != nullptr;
 
   int64_t n_mb = 0, sum_n = 0, raw = 0, rejected = 0;
@@ -70,92 +37,15 @@ __global__ __launch_bounds__(kWave) void k_epoch(EpochArgs a) {
     const int64_t se = min(sb + (int64_t)a.L, a.pos_end);
     const int len = (int)(se - sb);
     raw += len;
-
-    // 1. subsampling and compaction
-    int n_ret = 0;
-    for (int base = 0; base < len; base += kWave) {
-      const int off = base + lane;
-      const bool in = off < len;
-      const int x = in ? a.corpus[sb + off] : 0;
-      const bool bad = in && (x < 0 || x >= a.V);
-      bool keep = in && !bad;
-      if (keep && a.thr != nullptr) {
-        const U64x4 blk = stream_block(a.seed, (uint64_t)(sb + off), e, 0);
-        keep = (uint32_t)blk.v[0] <= a.thr[x];
-      }
-      const uint64_t m = __ballot(keep);
-      if (keep) {
-        const int dst = n_ret + __popcll(m & lanes_below(lane));
-        sl.ret_id[dst] = x;
-        sl.ret_off[dst] = (int16_t)off;
-      }
-      n_ret += __popcll(m);
-      rejected += __popcll(__ballot(bad));
-      if (kExport && in && !keep) a.out_targets[sb + off - a.pos_begin] = -1;
-    }
-    __syncthreads();
+    const int n_ret = keep_and_compact<kExport>(a, sb, len, lane, sl, rejected);
 
     for (int q0 = 0; q0 < n_ret; q0 += kWave) {
-      // 2. targets q0 .. q0+63, one per lane
-      const int q = q0 + lane;
-      if (q < n_ret) {
-        const int64_t p = sb + sl.ret_off[q];
-        const int t = sl.ret_id[q];
-        U64x4 blk = stream_block(a.seed, (uint64_t)p, e, 0);
-        const int h = w - (int)scale_draw(word_of(blk, 1), (uint64_t)w);
-        const int lo = max(q - h, 0);
-        const int hi = min(q + h, n_ret - 1);
-        const int n = hi - lo;
-        uint64_t mask = 0;
-        int bad = 0;
-        int cur = 0;
-        for (int k = 0; k < K; ++k) {
-          const int word = 2 + k;
-          if ((word >> 3) != cur) {
-            cur = word >> 3;
-            blk = stream_block(a.seed, (uint64_t)p, e, (uint64_t)cur);
-          }
-          const uint32_t r = word_of(blk, word & 7);
-          const int neg = a.table[scale_draw(r, (uint64_t)a.table_size)];
-          bad |= (neg < 0 || neg >= a.V);
-          if (neg == t) mask |= 1ull << k;
-          negs_lds[lane * K + k] = neg;
-        }
-        const float alpha = decayed_alpha(a.alpha0, a.min_frac, a.epoch,
-                                          a.n_epochs, a.T, p);
-        sl.lo[lane] = lo;
-        sl.n[lane] = n;
-        sl.alpha[lane] = alpha;
-        sl.mask[lane] = mask;
-        sl.bad[lane] = bad;
-        if constexpr (kExport) {
-          const int64_t r = p - a.pos_begin;
-          if (n == 0) {
-            a.out_targets[r] = -1;
-          } else {
-            a.out_targets[r] = t;
-            for (int i = 0; i < 2 * w; ++i) {
-              int id = -1;
-              if (i < n) {
-                const int jj = lo + i + (lo + i >= q ? 1 : 0);
-                id = sl.ret_id[jj];
-              }
-              a.out_ctx[r * 2 * w + i] = id;
-            }
-            for (int k = 0; k < K; ++k) {
-              a.out_negs[r * K + k] = negs_lds[lane * K + k];
-              a.out_mask[r * K + k] = (uint8_t)((mask >> k) & 1ull);
-            }
-            a.out_alpha[r] = alpha;
-          }
-        }
-      }
-      __syncthreads();
+      form_targets<kExport>(a, sb, q0, n_ret, lane, sl, tb, negs_lds);
       const int cnt = min(kWave, n_ret - q0);
       for (int j = 0; j < cnt; ++j) {
-        const int n = uniform_int(sl.n[j]);
+        const int n = uniform_int(tb.n[j]);
         if (n == 0) continue;
-        if (uniform_int(sl.bad[j]) != 0) {
+        if (uniform_int(tb.bad[j]) != 0) {
           ++rejected;
           continue;
         }
@@ -163,7 +53,7 @@ __global__ __launch_bounds__(kWave) void k_epoch(EpochArgs a) {
         sum_n += n;
         if constexpr (!kExport) {
           const int qj = q0 + j;
-          const int lo = uniform_int(sl.lo[j]);
+          const int lo = uniform_int(tb.lo[j]);
           int ctx_id = 0;
           if (lane < n) {
             int jj = lo + lane;
@@ -176,7 +66,7 @@ __global__ __launch_bounds__(kWave) void k_epoch(EpochArgs a) {
           float loss_part = 0.f;
           run_minibatch<C, NMAX, kMulti, true, false>(
               a.M_in, a.M_out, a.M_in, a.M_out, a.ld, a.D, lane, n_in, n_out,
-              uniform_float(sl.alpha[j]), a.hot_rows, mb, want_loss,
+              uniform_float(tb.alpha[j]), a.hot_rows, mb, want_loss,
               loss_part);
           if (want_loss) {
             const int64_t p = sb + sl.ret_off[qj];
@@ -194,12 +84,7 @@ __global__ __launch_bounds__(kWave) void k_epoch(EpochArgs a) {
     }
   }
   if (want_loss && bucket >= 0) flush_loss(a.loss, bucket, lsum, lcnt, lane);
-  if (a.stats != nullptr && lane == 0) {
-    atomicAdd((unsigned long long*)&a.stats[0], (unsigned long long)n_mb);
-    atomicAdd((unsigned long long*)&a.stats[1], (unsigned long long)sum_n);
-    atomicAdd((unsigned long long*)&a.stats[2], (unsigned long long)raw);
-    atomicAdd((unsigned long long*)&a.stats[3], (unsigned long long)rejected);
-  }
+  flush_stats(a.stats, lane, n_mb, sum_n, raw, rejected);
 }
 
 // ------------------------------------------------------------ launchers --

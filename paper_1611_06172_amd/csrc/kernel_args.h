@@ -63,5 +63,11 @@ bool train_shape_supported(int C, int nmax);
 int columns_for(int D);      // compiled C for a row length, 0 if none
 int inputs_cap_for(int n);   // compiled nmax for n input words, 0 if none
 int train_blocks_per_cu(int C, int nmax, int K);
+// Pipelined epoch kernel (single output block: K + 1 <= 64 / nmax).
+bool pipe_applies(int C, int nmax, int K);
+size_t pipe_dyn_lds(int C, int window, int K);
+int pipe_blocks_per_cu(int C, int nmax, int window, int K);
+hipError_t launch_pipe(int C, int nmax, const EpochArgs& a, int grid,
+                       hipStream_t s);
 
 }  // namespace w2v

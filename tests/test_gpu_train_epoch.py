@@ -93,6 +93,39 @@ def test_serialised_plain_and_mixed_update_paths(hot):
     assert rel_row_error(go, o_out) < 2e-4
 
 
+@pytest.mark.parametrize("kernel", ["pipe", "general"])
+@pytest.mark.parametrize("V,D,window,K,sub,L", [
+    (400, 64, 5, 5, 0.0, 1000),     # pipelined: one output block of 6
+    (600, 100, 2, 5, 1e-3, 257),    # small ring, ragged sentences
+    (300, 200, 8, 3, 0.0, 1000),    # window 8: 16 inputs, blocks of 4
+    (200, 72, 16, 1, 1e-2, 1024),   # window 16: 32 inputs, blocks of 2
+    (500, 300, 5, 0, 0.0, 50),      # no negatives, short sentences
+])
+def test_serialised_shapes_both_kernels(kernel, V, D, window, K, sub, L, monkeypatch):
+    """Serialised epochs of both epoch kernels against the oracle on the
+    shapes where the pipelined kernel applies (one output block)."""
+    monkeypatch.setenv("W2V_EPOCH_KERNEL", kernel)
+    corpus = inputs.zipf_ids(25_000, V, 1.0, V + window)
+    table, thr = oracle.build_tables(inputs.word_counts(corpus, V), 0.75, sub, 10**6)
+    if sub == 0.0:
+        thr = None
+    M_in = inputs.init_matrix(V, D, "uniform", 3)
+    M_out = inputs.init_matrix(V, D, "normal", 4, scale=0.05)
+    kw = dict(window=window, K=K, sentence_len=L, seed=5)
+    o_in, o_out = M_in.copy(), M_out.copy()
+    n, ob = oracle.train_epoch(oracle.Sampling(corpus, table, thr, **kw), o_in, o_out,
+                               n_buckets=3)
+    hot = 40 if window == 5 else None
+    gi, go, stats, gb = gpu_epoch(corpus, table, thr, M_in, M_out, n_buckets=3,
+                                  max_inflight=1, hot_rows=hot, **kw)
+    mb = oracle.minibatches(oracle.Sampling(corpus, table, thr, **kw))
+    assert stats[0] == n and stats[1] == (mb["ctx"] >= 0).sum()
+    assert rel_row_error(gi, o_in) < 2e-4
+    assert rel_row_error(go, o_out) < 2e-4
+    np.testing.assert_array_equal(gb[:, 1], ob[:, 1])
+    np.testing.assert_allclose(gb[:, 0], ob[:, 0], rtol=1e-5)
+
+
 def test_untouched_rows_unchanged():
     """Words absent from the corpus keep bitwise-identical rows."""
     V, D = 500, 64
