@@ -24,7 +24,7 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0   # MI355X HBM3E, 8 TB/s
 METRIC = "Mwords/sec at V=1M D=300 K=5 window=5 (1 GPU); achieved HBM GB/s"
 KERNEL_SOURCES = ["device_common.h", "sgns_core.h", "kernel_args.h",
-                  "sentence.h", "epoch_kernels.hip", "epoch_pipe.hip"]
+                  "sentence.h", "epoch_kernels.hip"]
 
 
 def kernel_hash():
@@ -65,6 +65,11 @@ def main():
                          "updated atomically (w2v_hot_rows)")
     ap.add_argument("--hot-rows", type=int, default=-1,
                     help="override the atomic-row threshold (-1: model)")
+    ap.add_argument("--split-tol", type=float, default=128.0,
+                    help="expected concurrent writers above which a row is "
+                         "spread over per-XCD partial rows (w2v_hot_rows)")
+    ap.add_argument("--split-rows", type=int, default=-1,
+                    help="override the split-row threshold (-1: model)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="run a 1 GiB device copy first (counter calibration)")
     ap.add_argument("--cpu-sample-tokens", type=int, default=1_000_000)
@@ -103,6 +108,13 @@ def main():
     hot = (args.hot_rows if args.hot_rows >= 0 else
            w2v.hot_rows(counts, sample_t=args.sample, window=W, K=K,
                         inflight=inflight, tol=args.hot_tol))
+    split = (args.split_rows if args.split_rows >= 0 else
+             w2v.hot_rows(counts, sample_t=args.sample, window=W, K=K,
+                          inflight=inflight, tol=args.split_tol))
+    ld = M_in.stride(0)
+    ws_bytes = w2v.train_epoch_workspace_bytes(split, ld)
+    workspace = (torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+                 if ws_bytes else None)
     if args.calibrate_copy:
         src = torch.empty(1 << 28, dtype=torch.float32, device=dev)
         src.fill_(1.0)
@@ -119,7 +131,7 @@ def main():
                         alpha0=0.025, min_alpha_frac=1e-4, epoch=i,
                         n_epochs=n_epochs, seed=1234, sentence_len=L,
                         stats=stats, max_inflight=args.max_inflight,
-                        hot_rows=hot)
+                        hot_rows=hot, split_rows=split, workspace=workspace)
 
     for i in range(args.warmup):
         step(i)
@@ -173,6 +185,7 @@ def main():
                          f"sentence {L}, alpha 0.025 linear"),
             "V": V, "T": T, "D": D, "K": K, "window": W, "sample": args.sample,
             "inflight_sentences": int(inflight), "atomic_rows": int(hot),
+            "split_rows": int(split),
             "minibatches_per_step": int(n_mb), "mean_inputs_per_minibatch":
                 round(sum_n / max(n_mb, 1), 4), "retained_fraction": round(n_mb / raw, 4),
         },

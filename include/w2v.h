@@ -56,6 +56,9 @@ extern "C" {
 #define W2V_MAX_SENTENCE 1024    /* sentence_len */
 #define W2V_MAX_BATCH_INPUTS 32  /* N of w2v_step_batch */
 
+/* Partial rows per split row of w2v_train_epoch (one per XCD of MI355X). */
+#define W2V_SPLIT_PARTS 8
+
 /* Version of this ABI (major * 100 + minor). */
 int w2v_version(void);
 
@@ -135,16 +138,6 @@ int64_t w2v_default_inflight(int32_t D, int32_t window, int32_t K);
  * to max_inflight sentences run concurrently and their updates interleave
  * without locks (Hogwild). max_inflight = 1 processes every minibatch in
  * sequence; 0 picks enough concurrent sentences to fill the GPU.
- * Two kernels implement this. The default loads and writes every row per
- * minibatch. An experimental pipelined kernel, selected by the environment
- * variable W2V_EPOCH_KERNEL=pipe where the K+1 output words fit one
- * reduction block (K + 1 <= 64 / (2 window) rounded to the compiled input
- * capacity), keeps each sentence's window of input rows in LDS, prefetches
- * one minibatch ahead and writes an input row of a word with id >= hot_rows
- * back once, when it leaves the window (its updates are summed there
- * first). Both keep the per-sentence order exact; the pipelined kernel
- * holds rare input rows longer, so more concurrent updates to them are
- * overwritten.
  * Update path: a row with id < hot_rows receives fp32 atomic adds (no update
  * is lost under concurrency); a row with id >= hot_rows is written back as
  * (value read + update) with a plain store, so a concurrent update of the
@@ -152,6 +145,17 @@ int64_t w2v_default_inflight(int32_t D, int32_t window, int32_t K);
  * ranked by frequency (id 0 the most frequent word) hot_rows selects the
  * frequent words, whose rows see concurrent updates; hot_rows >= V makes
  * every update atomic.
+ * Split rows: atomics are performed at the memory side and those to one
+ * address queue behind each other, so the few rows that nearly every
+ * concurrent sentence writes (the head of the Zipf law) would stall the
+ * whole memory system. A row with id < split_rows (regardless of hot_rows)
+ * is therefore spread over W2V_SPLIT_PARTS partial rows in `workspace`:
+ * each sentence adds its updates atomically to the partial row of its
+ * wavefront's group, every read of the row returns the matrix row plus all
+ * of its partial rows (so no update is hidden from any reader, as with a
+ * single atomic row), and after the epoch the partial rows are added into
+ * M_in/M_out and cleared. split_rows = 0 disables this; workspace may then
+ * be NULL.
  *
  * corpus: device int32[T]. [pos_begin, pos_end) must start on a sentence
  * boundary and end on one or at T. M_in, M_out: device, see conventions.
@@ -159,7 +163,12 @@ int64_t w2v_default_inflight(int32_t D, int32_t window, int32_t K);
  * loss_buckets: device double[2 * n_buckets] or NULL; for a minibatch of
  * target position p, bucket b = floor(p * n_buckets / T) receives
  * [2b] += sum_i [-log sigma(X_i0) - sum_{k unmasked} log sigma(-X_ik)] and
- * [2b+1] += N. stats: device int64[4] or NULL, accumulated into:
+ * [2b+1] += N. workspace: device memory of at least
+ * w2v_train_epoch_workspace_bytes(split_rows, ld) bytes, 256-byte aligned,
+ * caller-owned, its
+ * contents need not be initialised (the call clears what it uses), and it
+ * must not be shared by calls that overlap in time. stats: device int64[4]
+ * or NULL, accumulated into:
  * [0] minibatches applied, [1] sum of N over them, [2] raw positions
  * visited, [3] minibatches skipped for an id outside [0, V).
  * Limits: 1 <= D <= W2V_MAX_DIM, 1 <= window <= W2V_MAX_WINDOW,
@@ -173,7 +182,12 @@ int w2v_train_epoch(const int32_t* corpus, int64_t T, int64_t pos_begin,
                     float alpha0, float min_alpha_frac, int32_t epoch,
                     int32_t n_epochs, uint64_t seed, double* loss_buckets,
                     int32_t n_buckets, int64_t* stats, int32_t max_inflight,
-                    int32_t hot_rows, void* stream);
+                    int32_t hot_rows, int32_t split_rows, void* workspace,
+                    size_t workspace_bytes, void* stream);
+
+/* Workspace bytes w2v_train_epoch needs for split_rows rows of stride ld:
+ * 2 * split_rows * W2V_SPLIT_PARTS * ld * 4 (0 when split_rows is 0). */
+size_t w2v_train_epoch_workspace_bytes(int32_t split_rows, int32_t ld);
 
 /*
  * The minibatches w2v_train_epoch would form over [pos_begin, pos_end),

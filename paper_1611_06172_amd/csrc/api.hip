@@ -97,17 +97,9 @@ static int check_matrices(const float* M_in, const float* M_out, int32_t V,
   return W2V_OK;
 }
 
-// Epoch kernel choice: the general kernel, or the pipelined one where it
-// applies when the environment variable W2V_EPOCH_KERNEL is "pipe".
-static bool use_pipe(int C, int nmax, int K) {
-  const char* v = getenv("W2V_EPOCH_KERNEL");
-  if (v == nullptr || strcmp(v, "pipe") != 0) return false;
-  return pipe_applies(C, nmax, K);
-}
-
 static int epoch_blocks_per_cu(int C, int nmax, int window, int K) {
-  return use_pipe(C, nmax, K) ? pipe_blocks_per_cu(C, nmax, window, K)
-                              : train_blocks_per_cu(C, nmax, K);
+  (void)window;
+  return train_blocks_per_cu(C, nmax, K);
 }
 
 }  // namespace w2v
@@ -160,7 +152,8 @@ int w2v_train_epoch(const int32_t* corpus, int64_t T, int64_t pos_begin,
                     float alpha0, float min_alpha_frac, int32_t epoch,
                     int32_t n_epochs, uint64_t seed, double* loss_buckets,
                     int32_t n_buckets, int64_t* stats, int32_t max_inflight,
-                    int32_t hot_rows, void* stream) {
+                    int32_t hot_rows, int32_t split_rows, void* workspace,
+                    size_t workspace_bytes, void* stream) {
   int rc = check_sampling({corpus, T, pos_begin, pos_end, sentence_len, V,
                            window, K, neg_table, table_size, epoch, n_epochs});
   if (rc != W2V_OK) return rc;
@@ -170,6 +163,15 @@ int w2v_train_epoch(const int32_t* corpus, int64_t T, int64_t pos_begin,
     return fail(W2V_EINVAL, "n_buckets must be >= 1 with loss_buckets");
   if (max_inflight < 0) return fail(W2V_EINVAL, "max_inflight must be >= 0");
   if (hot_rows < 0) return fail(W2V_EINVAL, "hot_rows must be >= 0");
+  if (split_rows < 0 || split_rows > V)
+    return fail(W2V_EINVAL, "split_rows must be in [0, V]");
+  if (split_rows > 0) {
+    if (workspace == nullptr) return fail(W2V_EINVAL, "workspace is NULL");
+    if (workspace_bytes < w2v_train_epoch_workspace_bytes(split_rows, ld))
+      return fail(W2V_EINVAL, "workspace too small for split_rows");
+    if (((uintptr_t)workspace & 255u) != 0)
+      return fail(W2V_EINVAL, "workspace must be 256-byte aligned");
+  }
   const int C = columns_for(D);
   const int nmax = inputs_cap_for(2 * window);
   if (C == 0 || nmax == 0 || !train_shape_supported(C, nmax))
@@ -204,6 +206,8 @@ int w2v_train_epoch(const int32_t* corpus, int64_t T, int64_t pos_begin,
   a.n_buckets = n_buckets;
   a.stats = stats;
   a.hot_rows = hot_rows;
+  a.split_rows = split_rows;
+  a.part = (float*)workspace;
 
   int64_t grid = max_inflight;
   if (grid == 0) {
@@ -213,11 +217,25 @@ int w2v_train_epoch(const int32_t* corpus, int64_t T, int64_t pos_begin,
   }
   if (grid > n_sent) grid = n_sent;
   if (grid > (1 << 30)) grid = 1 << 30;
-  hipError_t e = use_pipe(C, nmax, K)
-                     ? launch_pipe(C, nmax, a, (int)grid, (hipStream_t)stream)
-                     : launch_train(C, nmax, a, (int)grid, (hipStream_t)stream);
+  hipStream_t s = (hipStream_t)stream;
+  hipError_t e = hipSuccess;
+  if (split_rows > 0) {
+    e = launch_part_clear(a, s);
+    if (e != hipSuccess) return hip_fail(e, "partial-row clear launch");
+  }
+  e = launch_train(C, nmax, a, (int)grid, s);
   if (e != hipSuccess) return hip_fail(e, "train kernel launch");
+  if (split_rows > 0) {
+    e = launch_part_fold(a, s);
+    if (e != hipSuccess) return hip_fail(e, "partial-row fold launch");
+  }
   return ok();
+}
+
+size_t w2v_train_epoch_workspace_bytes(int32_t split_rows, int32_t ld) {
+  if (split_rows <= 0 || ld <= 0) return 0;
+  return (size_t)2 * (size_t)split_rows * W2V_SPLIT_PARTS * (size_t)ld *
+         sizeof(float);
 }
 
 int w2v_debug_minibatches(const int32_t* corpus, int64_t T, int64_t pos_begin,

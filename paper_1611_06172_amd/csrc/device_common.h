@@ -161,23 +161,6 @@ __device__ __forceinline__ float wave_sum(float x) {
   return x;
 }
 
-// Orders LDS accesses between the lanes of a single-wavefront workgroup.
-// The LDS executes one wavefront's instructions in issue order, so the only
-// thing to prevent is the compiler moving LDS accesses across this point; a
-// workgroup barrier would also make the wavefront wait for all of its
-// outstanding global loads and stores.
-__device__ __forceinline__ void wave_sync() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-}
-
-// Waits until every global load, store and atomic of this wavefront has
-// completed (s_waitcnt vmcnt(0); expcnt and lgkmcnt left unconstrained).
-__device__ __forceinline__ void wait_global() {
-  __builtin_amdgcn_s_waitcnt(0x0F70);
-}
-
 __device__ __forceinline__ int uniform_int(int x) {
   return __builtin_amdgcn_readfirstlane(x);
 }
@@ -196,8 +179,13 @@ constexpr int kBufferWord3 = 0x00020000;
 // wavefronts (sc1: coherent at device scope).
 constexpr int kCoherentLoad = 16;
 
-// Cache policy of the plain (non-atomic) row stores of the Hogwild path.
-constexpr int kPlainStore = 0;
+// Cache policy of the plain (non-atomic) row stores of the Hogwild path:
+// sc1 writes through this XCD's L2, so wavefronts on other XCDs (whose
+// coherent loads do not see another XCD's L2) read the new row at once.
+// Without it a dirty line can stay in one XCD's L2 while other XCDs keep
+// reading and rewriting the old row, which overwrites far more updates than
+// the minibatch-long read-to-write window of Hogwild would.
+constexpr int kCoherentStore = 16;
 
 // Coherent (agent-scope) row element load and fp32 atomic add; used for the
 // live matrices that other wavefronts update concurrently.

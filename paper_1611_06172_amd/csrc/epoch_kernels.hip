@@ -9,9 +9,8 @@
 //      updates of the ones before it, while minibatches of different
 //      sentences interleave without locks (Hogwild, Sec. 1.1).
 // It serves every compiled shape, including output blocks that take several
-// reductions; the pipelined kernel (epoch_pipe.hip) serves the single-block
-// shapes. The export variant stops after step 2 and writes the minibatches
-// out.
+// reductions. The export variant stops after step 2 and writes the
+// minibatches out.
 #include "kernel_args.h"
 #include "sentence.h"
 #include "sgns_core.h"
@@ -67,7 +66,7 @@ __global__ __launch_bounds__(kWave) void k_epoch(EpochArgs a) {
           run_minibatch<C, NMAX, kMulti, true, false>(
               a.M_in, a.M_out, a.M_in, a.M_out, a.ld, a.D, lane, n_in, n_out,
               uniform_float(tb.alpha[j]), a.hot_rows, mb, want_loss,
-              loss_part);
+              loss_part, a.part, a.split_rows);
           if (want_loss) {
             const int64_t p = sb + sl.ret_off[qj];
             const int b = (int)(p * (int64_t)a.n_buckets / a.T);
@@ -87,7 +86,55 @@ __global__ __launch_bounds__(kWave) void k_epoch(EpochArgs a) {
   flush_stats(a.stats, lane, n_mb, sum_n, raw, rejected);
 }
 
+// Partial rows of the split rows: cleared before an epoch, summed (in the
+// order g = 0, 1, ...) and added into the matrices with one rounding, then
+// cleared, after it; a row with nothing pending keeps its bits. One thread
+// per (matrix, row, column).
+__global__ __launch_bounds__(256) void k_part_clear(EpochArgs a) {
+  const int64_t n = (int64_t)2 * a.split_rows * kSplitParts * a.ld;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x)
+    a.part[i] = 0.f;
+}
+
+__global__ __launch_bounds__(256) void k_part_fold(EpochArgs a) {
+  const int64_t n = (int64_t)2 * a.split_rows * a.D;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const int col = (int)(i % a.D);
+    const int64_t mr = i / a.D;  // m * split_rows + row
+    const int m = (int)(mr / a.split_rows);
+    const int64_t row = mr % a.split_rows;
+    float* pb = a.part + mr * kSplitParts * a.ld + col;
+    float* dst = (m == 0 ? a.M_in : a.M_out) + row * a.ld + col;
+    float sum = 0.f;
+    for (int g = 0; g < kSplitParts; ++g) {
+      sum += pb[g * a.ld];
+      pb[g * a.ld] = 0.f;
+    }
+    if (sum != 0.f) *dst += sum;
+  }
+}
+
 // ------------------------------------------------------------ launchers --
+
+static int part_grid(int64_t n) {
+  const int64_t b = (n + 255) / 256;
+  return (int)(b < 4096 ? (b > 0 ? b : 1) : 4096);
+}
+
+hipError_t launch_part_clear(const EpochArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(k_part_clear,
+                     dim3(part_grid((int64_t)2 * a.split_rows * kSplitParts * a.ld)),
+                     dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_part_fold(const EpochArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(k_part_fold, dim3(part_grid((int64_t)2 * a.split_rows * a.D)),
+                     dim3(256), 0, s, a);
+  return hipGetLastError();
+}
 
 #define W2V_TRAIN_SHAPES(X) \
   X(1, 10) X(2, 10) X(3, 10) X(4, 10) X(5, 10) X(6, 10) X(8, 10) X(10, 10) \

@@ -27,6 +27,8 @@ struct EpochArgs {
   int32_t n_buckets;
   int64_t* stats;          // NULL or int64[4]
   int32_t hot_rows;        // ids below this get atomic updates
+  int32_t split_rows;      // ids below this use partial rows in `part`
+  float* part;             // [2][split_rows][kSplitParts][ld] partial rows
   // export outputs (minibatch export only)
   int32_t* out_targets;
   int32_t* out_ctx;
@@ -57,17 +59,14 @@ struct StepArgs {
 hipError_t launch_train(int C, int nmax, const EpochArgs& a, int grid,
                         hipStream_t s);
 hipError_t launch_export(const EpochArgs& a, int grid, hipStream_t s);
+// Clears the partial rows / adds them into M_in, M_out and clears them.
+hipError_t launch_part_clear(const EpochArgs& a, hipStream_t s);
+hipError_t launch_part_fold(const EpochArgs& a, hipStream_t s);
 hipError_t launch_step(int C, int nmax, const StepArgs& a, int grid,
                        hipStream_t s);
 bool train_shape_supported(int C, int nmax);
 int columns_for(int D);      // compiled C for a row length, 0 if none
 int inputs_cap_for(int n);   // compiled nmax for n input words, 0 if none
 int train_blocks_per_cu(int C, int nmax, int K);
-// Pipelined epoch kernel (single output block: K + 1 <= 64 / nmax).
-bool pipe_applies(int C, int nmax, int K);
-size_t pipe_dyn_lds(int C, int window, int K);
-int pipe_blocks_per_cu(int C, int nmax, int window, int K);
-hipError_t launch_pipe(int C, int nmax, const EpochArgs& a, int grid,
-                       hipStream_t s);
 
 }  // namespace w2v

@@ -27,7 +27,13 @@
 // Update path (live matrices): rows with id < hot_rows receive fp32 atomic
 // adds (frequent words, whose concurrent updates would otherwise overwrite
 // each other), all other rows a plain store of (value read + update), the
-// Hogwild write the paper's threads perform (Sec. 1.1). Snapshot batches add
+// Hogwild write the paper's threads perform (Sec. 1.1). Rows below
+// split_rows (the head of the Zipf law, written by nearly every concurrent
+// wavefront) are spread over kSplitParts partial rows: a wavefront adds its
+// update atomically to the partial row of its group (blockIdx mod
+// kSplitParts, i.e. its XCD under round-robin dispatch), and reads return
+// the matrix row plus every partial row, so atomics to one address come from
+// one XCD only and nothing is hidden from a reader. Snapshot batches add
 // their updates with fp64 atomics into a delta buffer instead.
 //
 // Output columns are processed in blocks of KB = 64 / NMAX so that one
@@ -37,11 +43,13 @@
 #pragma once
 
 #include "device_common.h"
+#include "w2v.h"
 
 namespace w2v {
 
 constexpr int kMaxInputs = 32;   // input words per minibatch (2 * max window)
 constexpr int kMaxOutputs = 65;  // target + up to 64 negatives
+constexpr int kSplitParts = W2V_SPLIT_PARTS;
 
 // Per-wavefront LDS staging of one minibatch's ids and its error block.
 struct MinibatchLds {
@@ -161,7 +169,7 @@ __device__ __forceinline__ void update_row(void* base, int64_t id, int64_t ld,
       for (int c = 0; c < C; ++c)
         __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(old[c] + g[c]), rs,
                                               (lane + kWave * c) * 4, 0,
-                                              kPlainStore);
+                                              kCoherentStore);
     }
   }
 }
@@ -174,13 +182,41 @@ __device__ __forceinline__ float softplus(float z) {
 // Runs one minibatch. Rin/Rout: where rows are read; Win/Wout: where updates
 // go (the same fp32 matrices, or fp64 delta buffers with the same row stride
 // when kAccum64). n distinct input rows (n <= NMAX) in mb.ctx/mb.cwgt, n_out
-// distinct output columns in mb.out/mb.wgt. Every lane returns its share of
-// the minibatch loss in `loss_part` when want_loss is set.
+// distinct output columns in mb.out/mb.wgt. Rows id < split_rows of matrix m
+// (0: input, 1: output) have partial rows part[((m split_rows + id)
+// kSplitParts + g) ld], g < kSplitParts (live matrices only). Every lane
+// returns its share of the minibatch loss in `loss_part` when want_loss is
+// set.
 template <int C, int NMAX, bool kMulti, bool kLiveRead, bool kAccum64>
 __device__ __forceinline__ void run_minibatch(
     const float* Rin, const float* Rout, void* Win, void* Wout, int64_t ld,
     int D, int lane, int n, int n_out, float alpha, int hot_rows,
-    MinibatchLds& mb, bool want_loss, float& loss_part) {
+    MinibatchLds& mb, bool want_loss, float& loss_part,
+    float* part = nullptr, int split_rows = 0) {
+  auto part_base = [&](int m, int id) -> float* {
+    return part + (int64_t)(m * split_rows + id) * kSplitParts * ld;
+  };
+  // Adds the partial rows of a split row to its value as read.
+  auto read_split = [&](int m, int id, float (&r)[C]) {
+    if (id < split_rows) {
+      float* pb = part_base(m, id);
+      for (int g = 0; g < kSplitParts; ++g) {
+        float t[C];
+        load_row<C, true>(pb, g, ld, D, lane, t);
+#pragma unroll
+        for (int c = 0; c < C; ++c) r[c] += t[c];
+      }
+    }
+  };
+  auto update = [&](int m, void* W, int id, const float (&old)[C],
+                    const float (&g)[C]) {
+    if (id < split_rows) {
+      update_row<C, false>(part_base(m, id), blockIdx.x % kSplitParts, ld, D,
+                           lane, kSplitParts, old, g);
+    } else {
+      update_row<C, kAccum64>(W, id, ld, D, lane, hot_rows, old, g);
+    }
+  };
   constexpr int KB = kWave / NMAX;
   constexpr int kSlots = NMAX * KB;
   static_assert(KB >= 1 && kSlots <= kWave, "NMAX must be <= 64");
@@ -191,6 +227,7 @@ __device__ __forceinline__ void run_minibatch(
   for (int i = 0; i < NMAX; ++i) {
     if (i < n) {
       load_row<C, kLiveRead>(Rin, uniform_int(mb.ctx[i]), ld, D, lane, a[i]);
+      read_split(0, uniform_int(mb.ctx[i]), a[i]);
     } else {
 #pragma unroll
       for (int c = 0; c < C; ++c) a[i][c] = 0.f;
@@ -213,6 +250,7 @@ __device__ __forceinline__ void run_minibatch(
       if (k0 + kk < n_out) {
         load_row<C, kLiveRead>(Rout, uniform_int(mb.out[k0 + kk]), ld, D, lane,
                                o[kk]);
+        read_split(1, uniform_int(mb.out[k0 + kk]), o[kk]);
       } else {
 #pragma unroll
         for (int c = 0; c < C; ++c) o[kk][c] = 0.f;
@@ -269,8 +307,7 @@ __device__ __forceinline__ void run_minibatch(
             for (int c = 0; c < C; ++c) g[c] = fmaf(e, a[i][c], g[c]);
           }
         }
-        update_row<C, kAccum64>(Wout, uniform_int(mb.out[k]), ld, D, lane,
-                                hot_rows, o[kk], g);
+        update(1, Wout, uniform_int(mb.out[k]), o[kk], g);
       }
     }
 
@@ -291,8 +328,7 @@ __device__ __forceinline__ void run_minibatch(
 #pragma unroll
           for (int c = 0; c < C; ++c) ga[i][c] = g[c];
         } else {
-          update_row<C, kAccum64>(Win, uniform_int(mb.ctx[i]), ld, D, lane,
-                                  hot_rows, a[i], g);
+          update(0, Win, uniform_int(mb.ctx[i]), a[i], g);
         }
       }
     }
@@ -302,8 +338,7 @@ __device__ __forceinline__ void run_minibatch(
 #pragma unroll
     for (int i = 0; i < NMAX; ++i)
       if (i < n)
-        update_row<C, kAccum64>(Win, uniform_int(mb.ctx[i]), ld, D, lane,
-                                hot_rows, a[i], ga[i]);
+        update(0, Win, uniform_int(mb.ctx[i]), a[i], ga[i]);
   }
 }
 

@@ -56,8 +56,10 @@ def lib():
     L.w2v_train_epoch.argtypes = [
         _vp, _i64, _i64, _i64, _i32, _vp, _vp, _i32, _i32, _i32, _i32, _i32,
         _vp, _i64, _vp, _f32, _f32, _i32, _i32, _u64, _vp, _i32, _vp, _i32, _i32,
-        _vp]
+        _i32, _vp, ctypes.c_size_t, _vp]
     L.w2v_train_epoch.restype = ctypes.c_int
+    L.w2v_train_epoch_workspace_bytes.argtypes = [_i32, _i32]
+    L.w2v_train_epoch_workspace_bytes.restype = ctypes.c_size_t
     L.w2v_debug_minibatches.argtypes = [
         _vp, _i64, _i64, _i64, _i32, _i32, _i32, _i32, _vp, _i64, _vp, _f32,
         _f32, _i32, _i32, _u64, _vp, _vp, _vp, _vp, _vp, _vp, _vp]
@@ -137,8 +139,10 @@ def build_tables(counts, neg_power: float = 0.75, sample_t: float = 1e-4,
 
 
 def hot_rows(counts, *, neg_power: float = 0.75, sample_t: float = 1e-4,
-             window: int = 5, K: int = 5, inflight: int, tol: float = 0.5) -> int:
-    """Leading ids to update atomically (see w2v_hot_rows)."""
+             window: int = 5, K: int = 5, inflight: int, tol: float = 0.05) -> int:
+    """Leading ids to update atomically (see w2v_hot_rows). The default
+    tolerance keeps the expected share of overwritten updates of a plain row
+    near 5% (1 - exp(-tol))."""
     counts = np.ascontiguousarray(counts, dtype=np.int64)
     h = int(lib().w2v_hot_rows(counts.ctypes.data, counts.shape[0],
                                 float(neg_power), float(sample_t), window, K,
@@ -163,11 +167,14 @@ def train_epoch(corpus, M_in, M_out, neg_table, keep_thresh=None, *,
                 pos_begin: int = 0, pos_end: Optional[int] = None,
                 sentence_len: int = 1000, loss_buckets=None, stats=None,
                 max_inflight: int = 0, hot_rows: Optional[int] = None,
-                stream=None):
+                split_rows: int = 0, workspace=None, stream=None):
     """Hogwild HogBatch epoch over corpus[pos_begin:pos_end], in place.
 
     hot_rows: ids below it are updated with atomic adds, the others with
-    plain read-modify-write stores; None makes every update atomic."""
+    plain read-modify-write stores; None makes every update atomic.
+    split_rows: ids below it are updated through per-XCD partial rows that
+    every read sums (see w2v_train_epoch); workspace (a device byte tensor of
+    train_epoch_workspace_bytes(split_rows, ld)) is allocated when None."""
     import torch
     _dev(corpus, torch.int32, "corpus", 1)
     V, ld = _matrix(M_in, "M_in")
@@ -188,12 +195,24 @@ def train_epoch(corpus, M_in, M_out, neg_table, keep_thresh=None, *,
         _dev(stats, torch.int64, "stats", 1)
     T = corpus.numel()
     end = T if pos_end is None else pos_end
+    need = train_epoch_workspace_bytes(split_rows, ld)
+    if need and workspace is None:
+        workspace = torch.empty(need, dtype=torch.uint8, device=M_in.device)
+    ws_bytes = 0
+    if workspace is not None:
+        _dev(workspace, torch.uint8, "workspace", 1)
+        ws_bytes = workspace.numel()
     _check(lib().w2v_train_epoch(
         _ptr(corpus), T, pos_begin, end, sentence_len, _ptr(M_in), _ptr(M_out),
         V, D, ld, window, K, _ptr(neg_table), neg_table.numel(),
         _ptr(keep_thresh), alpha0, min_alpha_frac, epoch, n_epochs, seed,
         _ptr(loss_buckets), n_b, _ptr(stats), max_inflight,
-        V if hot_rows is None else int(hot_rows), _stream(stream)))
+        V if hot_rows is None else int(hot_rows), int(split_rows),
+        _ptr(workspace), ws_bytes, _stream(stream)))
+
+
+def train_epoch_workspace_bytes(split_rows: int, ld: int) -> int:
+    return int(lib().w2v_train_epoch_workspace_bytes(split_rows, ld))
 
 
 def debug_minibatches(corpus, neg_table, keep_thresh=None, *, V: int,

@@ -79,32 +79,32 @@ def test_serialised_with_subsampling_and_window_8():
     assert rel_row_error(go, o_out) < 2e-4
 
 
-@pytest.mark.parametrize("hot", [0, 37])
-def test_serialised_plain_and_mixed_update_paths(hot):
-    """Plain read-modify-write stores (ids >= hot) give the same serialised
-    result as atomics: within one wavefront nothing races."""
+@pytest.mark.parametrize("hot,split", [(0, 0), (37, 0), (37, 3), (0, 5), (1000, 1000)])
+def test_serialised_plain_mixed_and_split_update_paths(hot, split):
+    """Plain read-modify-write stores (ids >= hot), atomics and split rows
+    (ids < split, summed from partial rows and folded after the epoch) give
+    the same serialised result: within one wavefront nothing races, and a
+    split row reads back every update made to it."""
     corpus, table, M_in, M_out = tiny_config(T=30_000)
     kw = dict(window=5, K=5, sentence_len=1000, seed=11)
     o_in, o_out = M_in.copy(), M_out.copy()
     oracle.train_epoch(oracle.Sampling(corpus, table, None, **kw), o_in, o_out)
     gi, go, _, _ = gpu_epoch(corpus, table, None, M_in, M_out, max_inflight=1,
-                             hot_rows=hot, **kw)
+                             hot_rows=hot, split_rows=split, **kw)
     assert rel_row_error(gi, o_in) < 2e-4
     assert rel_row_error(go, o_out) < 2e-4
 
 
-@pytest.mark.parametrize("kernel", ["pipe", "general"])
 @pytest.mark.parametrize("V,D,window,K,sub,L", [
-    (400, 64, 5, 5, 0.0, 1000),     # pipelined: one output block of 6
+    (400, 64, 5, 5, 0.0, 1000),     # one output block of 6
     (600, 100, 2, 5, 1e-3, 257),    # small ring, ragged sentences
     (300, 200, 8, 3, 0.0, 1000),    # window 8: 16 inputs, blocks of 4
     (200, 72, 16, 1, 1e-2, 1024),   # window 16: 32 inputs, blocks of 2
     (500, 300, 5, 0, 0.0, 50),      # no negatives, short sentences
 ])
-def test_serialised_shapes_both_kernels(kernel, V, D, window, K, sub, L, monkeypatch):
-    """Serialised epochs of both epoch kernels against the oracle on the
-    shapes where the pipelined kernel applies (one output block)."""
-    monkeypatch.setenv("W2V_EPOCH_KERNEL", kernel)
+def test_serialised_shapes(V, D, window, K, sub, L):
+    """Serialised epochs against the oracle across input capacities, window
+    sizes, ragged sentences and the degenerate K = 0."""
     corpus = inputs.zipf_ids(25_000, V, 1.0, V + window)
     table, thr = oracle.build_tables(inputs.word_counts(corpus, V), 0.75, sub, 10**6)
     if sub == 0.0:
@@ -126,8 +126,10 @@ def test_serialised_shapes_both_kernels(kernel, V, D, window, K, sub, L, monkeyp
     np.testing.assert_allclose(gb[:, 0], ob[:, 0], rtol=1e-5)
 
 
-def test_untouched_rows_unchanged():
-    """Words absent from the corpus keep bitwise-identical rows."""
+@pytest.mark.parametrize("split", [0, 300])
+def test_untouched_rows_unchanged(split):
+    """Words absent from the corpus keep bitwise-identical rows, split rows
+    included."""
     V, D = 500, 64
     corpus = inputs.zipf_ids(20_000, 250, 1.0, 8)      # ids < 250 only
     table, _ = oracle.build_tables(inputs.word_counts(corpus, V), 0.75, 0.0, 10**6,
@@ -135,7 +137,7 @@ def test_untouched_rows_unchanged():
     M_in = inputs.init_matrix(V, D, "uniform", 9)
     M_out = inputs.init_matrix(V, D, "normal", 10, scale=0.01)
     gi, go, _, _ = gpu_epoch(corpus, table, None, M_in, M_out, window=5, K=5,
-                             sentence_len=1000)
+                             sentence_len=1000, split_rows=split)
     assert np.array_equal(gi[250:].view(np.uint32), M_in[250:].view(np.uint32))
     assert np.array_equal(go[250:].view(np.uint32), M_out[250:].view(np.uint32))
 
@@ -152,20 +154,29 @@ def eval_loss(M_in, M_out, t, c, n):
     return total / cnt
 
 
-@pytest.mark.parametrize("update_path", ["atomic", "model"])
+@pytest.mark.parametrize("update_path", ["atomic", "split", "model"])
 def test_hogwild_epoch_loss_within_2_percent(update_path):
-    corpus, table, M_in, M_out = tiny_config()
+    """Concurrent sentences against the sequential oracle: 200 sentences in
+    flight over 1,000 words (every row contended: all atomic, optionally the
+    head split into partial rows), or 64 in flight over 20,000 words with
+    the conflict model's plain rows."""
+    V, inflight = (1000, 0) if update_path != "model" else (20_000, 64)
+    corpus, table, M_in, M_out = tiny_config(T=200_000 if V == 1000 else 400_000, V=V)
     kw = dict(window=5, K=5, sentence_len=1000, seed=7, alpha0=0.025)
     o_in, o_out = M_in.copy(), M_out.copy()
     oracle.train_epoch(oracle.Sampling(corpus, table, None, **kw), o_in, o_out)
-    hot = None
+    counts = inputs.word_counts(corpus, V)
+    hot, split = None, 0
+    if update_path == "split":
+        split = w2v.hot_rows(counts, sample_t=0.0, inflight=200, tol=16.0)
+        assert 0 < split < 50
     if update_path == "model":
-        counts = inputs.word_counts(corpus, 1000)
-        hot = w2v.hot_rows(counts, sample_t=0.0, inflight=200, tol=0.5)
-        assert 0 < hot < 1000
-    gi, go, stats, _ = gpu_epoch(corpus, table, None, M_in, M_out, hot_rows=hot, **kw)
+        hot = w2v.hot_rows(counts, sample_t=0.0, inflight=inflight)
+        assert 0 < hot < V // 4
+    gi, go, stats, _ = gpu_epoch(corpus, table, None, M_in, M_out, hot_rows=hot,
+                                 split_rows=split, max_inflight=inflight, **kw)
     # held-out evaluation minibatches from the same unigram law
-    t, c, _ = inputs.kernel_batch(2000, 6, 5, 1000, 1.0, 99)
+    t, c, _ = inputs.kernel_batch(2000, 6, 5, V, 1.0, 99)
     n = table[np.random.default_rng(98).integers(0, len(table), (2000, 5))]
     lo = eval_loss(o_in, o_out, t, c, n)
     lg = eval_loss(gi, go, t, c, n)
