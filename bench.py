@@ -72,7 +72,7 @@ def main():
                     help="override the split-row threshold (-1: model)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="run a 1 GiB device copy first (counter calibration)")
-    ap.add_argument("--cpu-sample-tokens", type=int, default=1_000_000)
+    ap.add_argument("--cpu-sample-tokens", type=int, default=2_000_000)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--traffic-json",
                     default=os.path.join(ROOT, "profiles", "k_epoch_traffic.json"))
@@ -101,8 +101,9 @@ def main():
     table = torch.from_numpy(table_h).to(dev)
     thr = torch.from_numpy(thr_h.view(np.int32)).to(dev)
     M_in0 = inputs.init_matrix(V, D, "uniform", 2)
-    M_in = torch.from_numpy(M_in0).to(dev)
-    M_out = torch.zeros((V, D), dtype=torch.float32, device=dev)
+    # rows padded to whole 128-byte lines (ld = 320 floats at D = 300)
+    M_in = w2v.alloc_matrix(V, D, dev, torch.from_numpy(M_in0))
+    M_out = w2v.alloc_matrix(V, D, dev)
     stats = torch.zeros(4, dtype=torch.int64, device=dev)
     inflight = args.max_inflight or w2v.default_inflight(D, W, K)
     hot = (args.hot_rows if args.hot_rows >= 0 else
@@ -183,7 +184,7 @@ def main():
             "workload": (f"large-vocab HogBatch epoch: i.i.d. Zipf(1.07) corpus, "
                          f"T={T}, V={V}, D={D}, K={K}, window={W}, sample={args.sample}, "
                          f"sentence {L}, alpha 0.025 linear"),
-            "V": V, "T": T, "D": D, "K": K, "window": W, "sample": args.sample,
+            "V": V, "T": T, "D": D, "ld": ld, "K": K, "window": W, "sample": args.sample,
             "inflight_sentences": int(inflight), "atomic_rows": int(hot),
             "split_rows": int(split),
             "minibatches_per_step": int(n_mb), "mean_inputs_per_minibatch":

@@ -211,6 +211,25 @@ def train_epoch(corpus, M_in, M_out, neg_table, keep_thresh=None, *,
         _ptr(workspace), ws_bytes, _stream(stream)))
 
 
+def padded_ld(D: int) -> int:
+    """Row stride (floats) that starts every row on a 128-byte line: D
+    rounded up to a multiple of 32."""
+    return (D + 31) // 32 * 32
+
+
+def alloc_matrix(V: int, D: int, device="cuda", init=None):
+    """A (V, D) fp32 view of a zeroed (V, padded_ld(D)) device buffer,
+    optionally filled from `init` (array-like of shape (V, D)). Line-aligned
+    rows cost fewer partial-line reads and writes than a packed (V, D)
+    matrix when rows are gathered and scattered at random."""
+    import torch
+    buf = torch.zeros((V, padded_ld(D)), dtype=torch.float32, device=device)
+    M = buf[:, :D]
+    if init is not None:
+        M.copy_(torch.as_tensor(init))
+    return M
+
+
 def train_epoch_workspace_bytes(split_rows: int, ld: int) -> int:
     return int(lib().w2v_train_epoch_workspace_bytes(split_rows, ld))
 

@@ -154,13 +154,17 @@ def eval_loss(M_in, M_out, t, c, n):
     return total / cnt
 
 
-@pytest.mark.parametrize("update_path", ["atomic", "split", "model"])
-def test_hogwild_epoch_loss_within_2_percent(update_path):
-    """Concurrent sentences against the sequential oracle: 200 sentences in
+@pytest.mark.parametrize("update_path,inflight,bound", [
+    ("atomic", 64, 0.02), ("split", 64, 0.02), ("model", 64, 0.02),
+    ("atomic", 0, 0.05), ("split", 0, 0.05)])
+def test_hogwild_epoch_loss_near_sequential(update_path, inflight, bound):
+    """Concurrent sentences against the sequential oracle: 64 sentences in
     flight over 1,000 words (every row contended: all atomic, optionally the
-    head split into partial rows), or 64 in flight over 20,000 words with
-    the conflict model's plain rows."""
-    V, inflight = (1000, 0) if update_path != "model" else (20_000, 64)
+    head split into partial rows) or over 20,000 words with the conflict
+    model's plain rows, within 2% (observed: about 0.1%); all 200 sentences
+    at once over 1,000 words, where staleness is extreme, within 5%
+    (observed: about 1%)."""
+    V = 20_000 if update_path == "model" else 1000
     corpus, table, M_in, M_out = tiny_config(T=200_000 if V == 1000 else 400_000, V=V)
     kw = dict(window=5, K=5, sentence_len=1000, seed=7, alpha0=0.025)
     o_in, o_out = M_in.copy(), M_out.copy()
@@ -182,7 +186,7 @@ def test_hogwild_epoch_loss_within_2_percent(update_path):
     lg = eval_loss(gi, go, t, c, n)
     l0 = eval_loss(M_in, M_out, t, c, n)
     assert lo < 0.9 * l0                       # training moved the loss
-    assert abs(lg - lo) <= 0.02 * lo, (lg, lo, l0)
+    assert abs(lg - lo) <= bound * lo, (lg, lo, l0)
 
 
 def test_sentence_aligned_chunks_equal_one_call_when_serialised():
@@ -210,3 +214,27 @@ def test_validation_errors():
         w2v.train_epoch(c, M, M.clone(), tb, sentence_len=10, pos_begin=5)
     with pytest.raises(w2v.W2VError):
         w2v.train_epoch(c, M, M.clone(), tb, K=65)
+
+
+def test_padded_rows_match_packed_rows_bitwise():
+    """A line-aligned row stride (w2v.alloc_matrix) changes where rows live,
+    not the arithmetic: the serialised epoch is bitwise the same as with
+    packed rows, and the padding columns are never written."""
+    import torch
+    V, D = 500, 300
+    corpus = inputs.zipf_ids(20_000, V, 1.0, 12)
+    table, _ = oracle.build_tables(inputs.word_counts(corpus, V), 0.75, 0.0, 10**6,
+                                   want_thresh=False)
+    M_in = inputs.init_matrix(V, D, "uniform", 13)
+    M_out = inputs.init_matrix(V, D, "normal", 14, scale=0.01)
+    kw = dict(window=5, K=5, sentence_len=1000, seed=15, max_inflight=1, split_rows=2)
+    a_in, a_out, _, _ = gpu_epoch(corpus, table, None, M_in, M_out, **kw)
+    p_in = w2v.alloc_matrix(V, D, "cuda", torch.from_numpy(M_in))
+    p_out = w2v.alloc_matrix(V, D, "cuda", torch.from_numpy(M_out))
+    assert p_in.stride(0) == 320
+    w2v.train_epoch(to_dev(corpus), p_in, p_out, to_dev(table), None, **kw)
+    torch.cuda.synchronize()
+    assert np.array_equal(p_in.cpu().numpy().view(np.uint32), a_in.view(np.uint32))
+    assert np.array_equal(p_out.cpu().numpy().view(np.uint32), a_out.view(np.uint32))
+    full = torch.as_strided(p_in, (V, 320), (320, 1)).cpu().numpy()
+    assert not full[:, D:].any()
