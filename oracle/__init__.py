@@ -79,6 +79,13 @@ def lib():
                                          ctypes.c_int32, ctypes.c_int32,
                                          ctypes.c_int32, _f64p, ctypes.c_int32]
         L.oracle_train_epoch.restype = ctypes.c_int64
+        L.oracle_pair_negative.argtypes = [ctypes.POINTER(_Sampling), ctypes.c_int64,
+                                           ctypes.c_int32, ctypes.c_int32]
+        L.oracle_pair_negative.restype = ctypes.c_int32
+        L.oracle_pairwise_train_epoch.argtypes = [ctypes.POINTER(_Sampling), _f32p,
+                                                  _f32p, ctypes.c_int32, ctypes.c_int32,
+                                                  ctypes.c_int32, _f64p, ctypes.c_int32]
+        L.oracle_pairwise_train_epoch.restype = ctypes.c_int64
         _lib = L
     return _lib
 
@@ -284,4 +291,32 @@ def train_epoch(s: Sampling, M_in, M_out, D=None, n_buckets=0):
                                  _ptr(buckets, _f64p), n_buckets)
     if n < 0:
         raise ValueError("oracle_train_epoch failed")
+    return n, buckets
+
+
+def pair_negatives(s: Sampling, p: int, n_inputs: int) -> np.ndarray:
+    """[n_inputs, K] negatives of Algorithm 1 for the target at raw position
+    p: row i holds the K draws of input word i."""
+    st = s._struct()
+    out = np.empty((n_inputs, s.K), dtype=np.int32)
+    for i in range(n_inputs):
+        for k in range(s.K):
+            out[i, k] = lib().oracle_pair_negative(ctypes.byref(st), p, i, k)
+    return out
+
+
+def pairwise_train_epoch(s: Sampling, M_in, M_out, D=None, n_buckets=0):
+    """Algorithm 1 (per-pair Hogwild SGD), sequential, in place on fp32
+    matrices. Returns (targets applied, loss_buckets[n_buckets, 2] or None)."""
+    assert M_in.dtype == np.float32 and M_in.flags.c_contiguous
+    assert M_out.dtype == np.float32 and M_out.flags.c_contiguous
+    V, ld = M_in.shape
+    D = ld if D is None else D
+    st = s._struct()
+    buckets = np.zeros((n_buckets, 2)) if n_buckets > 0 else None
+    n = lib().oracle_pairwise_train_epoch(ctypes.byref(st), _ptr(M_in, _f32p),
+                                          _ptr(M_out, _f32p), V, D, ld,
+                                          _ptr(buckets, _f64p), n_buckets)
+    if n < 0:
+        raise ValueError("oracle_pairwise_train_epoch failed")
     return n, buckets

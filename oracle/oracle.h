@@ -133,6 +133,21 @@ int64_t oracle_train_epoch(const oracle_sampling* s, float* M_in, float* M_out,
                            int32_t V, int32_t D, int32_t ld,
                            double* loss_buckets, int32_t n_buckets);
 
+/* Algorithm 1 (per-pair Hogwild SGD, one thread), sequential over the same
+ * minibatches as oracle_train_epoch (targets, input words in window order,
+ * learning rates), each input word with K negatives of its own:
+ * oracle_pair_negative(s, p, i, k) is negative k of input word i of the
+ * target at raw position p (draw 2 + iK + k of its stream). Returns the
+ * number of targets applied, < 0 on bad arguments or an id outside [0, V).
+ * Loss buckets as in oracle_train_epoch (the pairs' losses at the moment of
+ * each pair). */
+int32_t oracle_pair_negative(const oracle_sampling* s, int64_t p, int32_t i,
+                             int32_t k);
+int64_t oracle_pairwise_train_epoch(const oracle_sampling* s, float* M_in,
+                                    float* M_out, int32_t V, int32_t D,
+                                    int32_t ld, double* loss_buckets,
+                                    int32_t n_buckets);
+
 #ifdef __cplusplus
 }
 #endif

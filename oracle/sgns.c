@@ -314,3 +314,111 @@ int64_t oracle_train_epoch(const oracle_sampling* s, float* M_in, float* M_out,
   oracle_sentence_free(&sen);
   return status == 0 ? applied : -1;
 }
+
+/*
+ * Algorithm 1 (the original Hogwild SGD of word2vec, one thread), sequential.
+ * For one target word and its input words in window order, each input word i
+ * runs its own K+1 logistic regressions: the target (label 1) and K
+ * negatives of its own (label 0; a draw equal to the target is skipped).
+ * Every inner product uses the M_out row as it is at that moment (it was
+ * moved by the previous pairs), the M_out row moves right after its pair,
+ * and the M_in row of i moves once, after its K+1 pairs, by the sum of
+ * alpha * error * (M_out row as used). Reading: the negatives of input word
+ * i are the draws 2 + iK .. 2 + iK + K - 1 of the target's random stream, so
+ * input word 0 draws exactly the negatives a HogBatch minibatch shares.
+ * Arithmetic in fp64 from the stored fp32 values; each row update is
+ * rounded to fp32 when it is written.
+ */
+int32_t oracle_pair_negative(const oracle_sampling* s, int64_t p, int32_t i,
+                             int32_t k) {
+  uint32_t word = 2u + (uint32_t)i * (uint32_t)s->K + (uint32_t)k;
+  uint32_t r = oracle_draw_u32(s->seed, (uint64_t)p, (uint64_t)s->epoch, word);
+  return s->neg_table[((uint64_t)r * (uint64_t)s->table_size) >> 32];
+}
+
+/* One target: returns -1 when an id is out of range (nothing is applied),
+ * else 0; adds the pairs' losses to *loss. */
+static int alg1_target(const oracle_sampling* s, float* M_in, float* M_out,
+                       int32_t V, int32_t D, int32_t ld, int64_t p,
+                       int32_t target, const int32_t* ctx, int32_t n,
+                       float alpha, double* a, double* o, double* temp,
+                       double* loss) {
+  if (target < 0 || target >= V) return -1;
+  for (int32_t i = 0; i < n; ++i) {
+    if (ctx[i] < 0 || ctx[i] >= V) return -1;
+    for (int32_t k = 0; k < s->K; ++k) {
+      int32_t neg = oracle_pair_negative(s, p, i, k);
+      if (neg < 0 || neg >= V) return -1;
+    }
+  }
+  for (int32_t i = 0; i < n; ++i) {
+    float* in_row = M_in + (size_t)ctx[i] * ld;
+    for (int32_t j = 0; j < D; ++j) {
+      a[j] = (double)in_row[j];
+      temp[j] = 0.0;
+    }
+    for (int32_t k = 0; k <= s->K; ++k) {
+      int32_t word = target;
+      double label = 1.0;
+      if (k > 0) {
+        word = oracle_pair_negative(s, p, i, k - 1);
+        label = 0.0;
+        if (word == target) continue;
+      }
+      float* out_row = M_out + (size_t)word * ld;
+      double inner = 0.0;
+      for (int32_t j = 0; j < D; ++j) {
+        o[j] = (double)out_row[j];
+        inner += a[j] * o[j];
+      }
+      double err = (double)alpha * (label - sigma(inner));
+      *loss -= log_sigma(label > 0.0 ? inner : -inner);
+      for (int32_t j = 0; j < D; ++j) {
+        temp[j] += err * o[j];
+        out_row[j] = (float)(o[j] + err * a[j]);
+      }
+    }
+    for (int32_t j = 0; j < D; ++j) in_row[j] = (float)(a[j] + temp[j]);
+  }
+  return 0;
+}
+
+int64_t oracle_pairwise_train_epoch(const oracle_sampling* s, float* M_in,
+                                    float* M_out, int32_t V, int32_t D,
+                                    int32_t ld, double* loss_buckets,
+                                    int32_t n_buckets) {
+  if (oracle_validate_sampling(s) != 0) return -1;
+  if (M_in == NULL || M_out == NULL || V <= 0 || D <= 0 || ld < D) return -1;
+  if (loss_buckets != NULL && n_buckets <= 0) return -1;
+  oracle_sentence sen;
+  if (oracle_sentence_alloc(&sen, s->sentence_len, s->window, s->K) != 0)
+    return -2;
+  double* a = (double*)malloc(sizeof(double) * (size_t)D);
+  double* o = (double*)malloc(sizeof(double) * (size_t)D);
+  double* temp = (double*)malloc(sizeof(double) * (size_t)D);
+  const int32_t w2 = 2 * s->window;
+  int64_t applied = 0;
+  int status = (a && o && temp) ? 0 : -2;
+  for (int64_t sb = s->pos_begin; sb < s->pos_end && status == 0;
+       sb += s->sentence_len) {
+    int64_t se = sb + s->sentence_len;
+    if (se > s->T) se = s->T;
+    int32_t n_mb = oracle_sentence_minibatches(s, sb, se, &sen);
+    for (int32_t m = 0; m < n_mb; ++m) {
+      double loss = 0.0;
+      status = alg1_target(s, M_in, M_out, V, D, ld, sen.pos[m], sen.target[m],
+                           sen.ctx + (size_t)m * w2, sen.n_ctx[m], sen.alpha[m],
+                           a, o, temp, &loss);
+      if (status != 0) break;
+      if (loss_buckets != NULL) {
+        int64_t b = sen.pos[m] * (int64_t)n_buckets / s->T;
+        loss_buckets[2 * b] += loss;
+        loss_buckets[2 * b + 1] += (double)sen.n_ctx[m];
+      }
+      ++applied;
+    }
+  }
+  free(a); free(o); free(temp);
+  oracle_sentence_free(&sen);
+  return status == 0 ? applied : status;
+}
