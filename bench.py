@@ -60,6 +60,9 @@ def main():
     ap.add_argument("--window", type=int, default=5)
     ap.add_argument("--sample", type=float, default=1e-4)
     ap.add_argument("--max-inflight", type=int, default=0)
+    ap.add_argument("--algorithm", choices=["hogbatch", "pairwise"], default="hogbatch",
+                    help="hogbatch (Sec. 1.1, the measured path) or pairwise "
+                         "(Alg. 1, the paper's baseline, for comparison)")
     ap.add_argument("--hot-tol", type=float, default=0.5,
                     help="expected concurrent writers above which a row is "
                          "updated atomically (w2v_hot_rows)")
@@ -112,6 +115,8 @@ def main():
     split = (args.split_rows if args.split_rows >= 0 else
              w2v.hot_rows(counts, sample_t=args.sample, window=W, K=K,
                           inflight=inflight, tol=args.split_tol))
+    if args.algorithm == "pairwise":
+        split = 0  # partial rows serve the HogBatch kernel only
     ld = M_in.stride(0)
     ws_bytes = w2v.train_epoch_workspace_bytes(split, ld)
     workspace = (torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
@@ -132,7 +137,8 @@ def main():
                         alpha0=0.025, min_alpha_frac=1e-4, epoch=i,
                         n_epochs=n_epochs, seed=1234, sentence_len=L,
                         stats=stats, max_inflight=args.max_inflight,
-                        hot_rows=hot, split_rows=split, workspace=workspace)
+                        hot_rows=hot, split_rows=split, workspace=workspace,
+                        algorithm=args.algorithm)
 
     for i in range(args.warmup):
         step(i)
@@ -158,14 +164,19 @@ def main():
 
     ms_per_step = wall * 1e3 / args.steps
     words_per_s = T / (wall / args.steps)
-    # Algorithmic bytes per launch: every minibatch gathers and writes back its
-    # N + K + 1 rows (8 D bytes per row) and reads K table entries; every raw
-    # word reads its id and its keep threshold.
+    # Algorithmic bytes per launch: every HogBatch minibatch gathers and writes
+    # back its N + K + 1 rows (8 D bytes per row) and reads K table entries;
+    # Algorithm 1 moves, per input word, its own row and K + 1 output rows and
+    # reads K table entries; every raw word reads its id and keep threshold.
     n_mb, sum_n, raw = st[0], st[1], st[2]
-    alg_bytes = 8.0 * D * (sum_n + n_mb * (K + 1)) + 4.0 * K * n_mb + 8.0 * raw
+    if args.algorithm == "pairwise":
+        alg_bytes = 8.0 * D * sum_n * (K + 2) + 4.0 * K * sum_n + 8.0 * raw
+    else:
+        alg_bytes = 8.0 * D * (sum_n + n_mb * (K + 1)) + 4.0 * K * n_mb + 8.0 * raw
     avg_kern_s = float(np.mean(kern_ms)) / 1e3
     achieved = alg_bytes / avg_kern_s / 1e9
-    traffic = measured_traffic(args.traffic_json, 1.0)
+    traffic = (measured_traffic(args.traffic_json, 1.0)
+               if args.algorithm == "hogbatch" else None)
 
     result = {
         "metric": METRIC,
@@ -181,7 +192,8 @@ def main():
         "dtype": "f32",
         "data": "synthetic",
         "config": {
-            "workload": (f"large-vocab HogBatch epoch: i.i.d. Zipf(1.07) corpus, "
+            "workload": (f"large-vocab {'Algorithm 1 (per-pair)' if args.algorithm == 'pairwise' else 'HogBatch'} "
+                         f"epoch: i.i.d. Zipf(1.07) corpus, "
                          f"T={T}, V={V}, D={D}, K={K}, window={W}, sample={args.sample}, "
                          f"sentence {L}, alpha 0.025 linear"),
             "V": V, "T": T, "D": D, "ld": ld, "K": K, "window": W, "sample": args.sample,
@@ -192,7 +204,7 @@ def main():
         },
         "roofline": {
             "bound": "hbm",
-            "kernel": "k_epoch",
+            "kernel": "k_epoch_pairwise" if args.algorithm == "pairwise" else "k_epoch",
             "achieved": round(achieved, 1),
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
@@ -212,7 +224,8 @@ def main():
         s = oracle.Sampling(sample_corpus, table_h, thr_h, window=W, K=K,
                             sentence_len=L, seed=1234)
         c0 = time.perf_counter()
-        n_o, _ = oracle.train_epoch(s, o_in, o_out)
+        run = oracle.pairwise_train_epoch if args.algorithm == "pairwise" else oracle.train_epoch
+        n_o, _ = run(s, o_in, o_out)
         c_dt = time.perf_counter() - c0
         result["cpu_baseline"] = {
             "value": round(n_s / c_dt / 1e6, 5),

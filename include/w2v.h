@@ -59,6 +59,10 @@ extern "C" {
 /* Partial rows per split row of w2v_train_epoch (one per XCD of MI355X). */
 #define W2V_SPLIT_PARTS 8
 
+/* The `algorithm` argument of w2v_train_epoch. */
+#define W2V_ALGORITHM_HOGBATCH 0  /* Sec. 1.1: minibatch, shared negatives */
+#define W2V_ALGORITHM_PAIRWISE 1  /* Alg. 1: per-pair SGD, private negatives */
+
 /* Version of this ABI (major * 100 + minor). */
 int w2v_version(void);
 
@@ -138,10 +142,20 @@ int64_t w2v_default_inflight(int32_t D, int32_t window, int32_t K);
  * to max_inflight sentences run concurrently and their updates interleave
  * without locks (Hogwild). max_inflight = 1 processes every minibatch in
  * sequence; 0 picks enough concurrent sentences to fill the GPU.
+ * algorithm = W2V_ALGORITHM_PAIRWISE runs Alg. 1 instead (the original
+ * per-pair Hogwild SGD, the paper's baseline) over the same targets, input
+ * words and learning rates: each input word i in window order runs K+1
+ * logistic regressions against the target and K negatives of its own
+ * (draws 2 + iK + k of the target's stream; a draw equal to the target is
+ * skipped); each pair reads the M_out row as moved by the pairs before it,
+ * that row moves right after its pair, and the M_in row of i moves once,
+ * after its K+1 pairs. A target with any negative outside [0, V) is skipped
+ * and counted in stats[3]. split_rows must be 0 with this algorithm.
  * Update path: a row with id < hot_rows receives fp32 atomic adds (no update
  * is lost under concurrency); a row with id >= hot_rows is written back as
- * (value read + update) with a plain store, so a concurrent update of the
- * same row by another sentence may be overwritten, as in Hogwild. With ids
+ * (value read + update) by a store written through to device scope, so a
+ * concurrent update of the same row by another sentence may be
+ * overwritten, as in Hogwild. With ids
  * ranked by frequency (id 0 the most frequent word) hot_rows selects the
  * frequent words, whose rows see concurrent updates; hot_rows >= V makes
  * every update atomic.
@@ -183,7 +197,7 @@ int w2v_train_epoch(const int32_t* corpus, int64_t T, int64_t pos_begin,
                     int32_t n_epochs, uint64_t seed, double* loss_buckets,
                     int32_t n_buckets, int64_t* stats, int32_t max_inflight,
                     int32_t hot_rows, int32_t split_rows, void* workspace,
-                    size_t workspace_bytes, void* stream);
+                    size_t workspace_bytes, int32_t algorithm, void* stream);
 
 /* Workspace bytes w2v_train_epoch needs for split_rows rows of stride ld:
  * 2 * split_rows * W2V_SPLIT_PARTS * ld * 4 (0 when split_rows is 0). */

@@ -16,7 +16,8 @@ BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libw2v.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
-HIP_SOURCES = ["api.hip", "epoch_kernels.hip", "step_kernels.hip"]
+HIP_SOURCES = ["api.hip", "epoch_kernels.hip", "pairwise_kernels.hip",
+               "step_kernels.hip"]
 CXX_SOURCES = ["tables.cpp"]
 
 HIP_FLAGS = [

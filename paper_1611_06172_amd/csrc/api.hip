@@ -153,7 +153,7 @@ int w2v_train_epoch(const int32_t* corpus, int64_t T, int64_t pos_begin,
                     int32_t n_epochs, uint64_t seed, double* loss_buckets,
                     int32_t n_buckets, int64_t* stats, int32_t max_inflight,
                     int32_t hot_rows, int32_t split_rows, void* workspace,
-                    size_t workspace_bytes, void* stream) {
+                    size_t workspace_bytes, int32_t algorithm, void* stream) {
   int rc = check_sampling({corpus, T, pos_begin, pos_end, sentence_len, V,
                            window, K, neg_table, table_size, epoch, n_epochs});
   if (rc != W2V_OK) return rc;
@@ -163,8 +163,12 @@ int w2v_train_epoch(const int32_t* corpus, int64_t T, int64_t pos_begin,
     return fail(W2V_EINVAL, "n_buckets must be >= 1 with loss_buckets");
   if (max_inflight < 0) return fail(W2V_EINVAL, "max_inflight must be >= 0");
   if (hot_rows < 0) return fail(W2V_EINVAL, "hot_rows must be >= 0");
+  if (algorithm != W2V_ALGORITHM_HOGBATCH && algorithm != W2V_ALGORITHM_PAIRWISE)
+    return fail(W2V_EINVAL, "algorithm must be W2V_ALGORITHM_HOGBATCH or _PAIRWISE");
   if (split_rows < 0 || split_rows > V)
     return fail(W2V_EINVAL, "split_rows must be in [0, V]");
+  if (algorithm == W2V_ALGORITHM_PAIRWISE && split_rows != 0)
+    return fail(W2V_EINVAL, "split_rows must be 0 with the pairwise algorithm");
   if (split_rows > 0) {
     if (workspace == nullptr) return fail(W2V_EINVAL, "workspace is NULL");
     if (workspace_bytes < w2v_train_epoch_workspace_bytes(split_rows, ld))
@@ -209,9 +213,11 @@ int w2v_train_epoch(const int32_t* corpus, int64_t T, int64_t pos_begin,
   a.split_rows = split_rows;
   a.part = (float*)workspace;
 
+  const bool pairwise = algorithm == W2V_ALGORITHM_PAIRWISE;
   int64_t grid = max_inflight;
   if (grid == 0) {
-    const int per_cu = epoch_blocks_per_cu(C, nmax, window, K);
+    const int per_cu = pairwise ? pairwise_blocks_per_cu(C, K)
+                                : epoch_blocks_per_cu(C, nmax, window, K);
     const int cus = cu_count();
     grid = (int64_t)(per_cu > 0 ? per_cu : 1) * (cus > 0 ? cus : 1);
   }
@@ -223,7 +229,8 @@ int w2v_train_epoch(const int32_t* corpus, int64_t T, int64_t pos_begin,
     e = launch_part_clear(a, s);
     if (e != hipSuccess) return hip_fail(e, "partial-row clear launch");
   }
-  e = launch_train(C, nmax, a, (int)grid, s);
+  e = pairwise ? launch_pairwise(C, a, (int)grid, s)
+               : launch_train(C, nmax, a, (int)grid, s);
   if (e != hipSuccess) return hip_fail(e, "train kernel launch");
   if (split_rows > 0) {
     e = launch_part_fold(a, s);

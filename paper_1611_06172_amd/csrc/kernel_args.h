@@ -68,5 +68,8 @@ bool train_shape_supported(int C, int nmax);
 int columns_for(int D);      // compiled C for a row length, 0 if none
 int inputs_cap_for(int n);   // compiled nmax for n input words, 0 if none
 int train_blocks_per_cu(int C, int nmax, int K);
+// Algorithm 1 (per-pair) epoch kernel.
+int pairwise_blocks_per_cu(int C, int K);
+hipError_t launch_pairwise(int C, const EpochArgs& a, int grid, hipStream_t s);
 
 }  // namespace w2v

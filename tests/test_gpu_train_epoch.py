@@ -165,7 +165,10 @@ def test_hogwild_epochs_near_sequential(update_path, inflight, bound):
     words, where staleness is extreme, within 5% (observed: about 1%).
     Compared: the training-loss trajectory (mean loss per input word of each
     epoch, as the minibatches were applied) and the held-out loss of the
-    final model. Loss by raw position inside one epoch is not compared: the
+    final model. With the whole corpus in flight, every sentence of epoch 0
+    starts from the initial model, so that epoch's training loss is not
+    comparable (observed 9% above the sequential one) and the trajectory is
+    compared from epoch 1. Loss by raw position inside one epoch is not compared: the
     concurrent schedule visits the sentences of a position range at other
     model states than the sequential one."""
     import torch
@@ -197,7 +200,8 @@ def test_hogwild_epochs_near_sequential(update_path, inflight, bound):
         traj_g.append(gb[0, 0] / gb[0, 1])
     traj_o, traj_g = np.array(traj_o), np.array(traj_g)
     assert traj_o[-1] < traj_o[0]                       # training moved the loss
-    assert np.all(np.abs(traj_g - traj_o) <= bound * traj_o), (traj_g, traj_o)
+    first = 1 if inflight == 0 else 0
+    assert np.all(np.abs(traj_g - traj_o)[first:] <= bound * traj_o[first:]), (traj_g, traj_o)
     # held-out evaluation minibatches from the same unigram law
     t, ctx, _ = inputs.kernel_batch(2000, 6, 5, V, 1.0, 99)
     negs = table[np.random.default_rng(98).integers(0, len(table), (2000, 5))]
