@@ -131,10 +131,9 @@ __device__ __forceinline__ float f_pair_dpp(float a, float b, bool upper) {
 // Transposing reduction of 64 values per lane. On return, lane l holds
 // sum over all 64 lanes of v[l]. The partner of each step differs from the
 // lane in exactly the bit being split (32, 16, then 8, 4, 2, 1 via mirrors),
-// so the six steps together cover every lane once.
-__device__ __forceinline__ float xpose_reduce64(float (&v)[64], int lane) {
-#pragma unroll
-  for (int j = 0; j < 32; ++j) v[j] = f_swap_sum32(v[j], v[j + 32]);
+// so the six steps together cover every lane once. The steps after the
+// first (32 values left):
+__device__ __forceinline__ float xpose_tail32(float (&v)[32], int lane) {
 #pragma unroll
   for (int j = 0; j < 16; ++j) v[j] = f_swap_sum16(v[j], v[j + 16]);
   const bool b3 = (lane & 8) != 0;
@@ -150,6 +149,25 @@ __device__ __forceinline__ float xpose_reduce64(float (&v)[64], int lane) {
   return f_pair_dpp<kDppXor1>(v[0], v[1], b0);
 }
 
+__device__ __forceinline__ float xpose_reduce64(float (&v)[64], int lane) {
+  float w[32];
+#pragma unroll
+  for (int j = 0; j < 32; ++j) w[j] = f_swap_sum32(v[j], v[j + 32]);
+  return xpose_tail32(w, lane);
+}
+
+// The same reduction with value s produced on demand by value(s) (s a
+// compile-time index after unrolling), so that values s and s + 32 are
+// formed just before the first step combines them and at most 32 partial
+// sums are live at once.
+template <class F>
+__device__ __forceinline__ float xpose_reduce64_lazy(F&& value, int lane) {
+  float w[32];
+#pragma unroll
+  for (int j = 0; j < 32; ++j) w[j] = f_swap_sum32(value(j), value(j + 32));
+  return xpose_tail32(w, lane);
+}
+
 // Sum of one float over the wave (every lane gets the total).
 __device__ __forceinline__ float wave_sum(float x) {
   x += __shfl_xor(x, 32);
@@ -159,6 +177,12 @@ __device__ __forceinline__ float wave_sum(float x) {
   x += __shfl_xor(x, 2);
   x += __shfl_xor(x, 1);
   return x;
+}
+
+// Value of x in lane l (l uniform; a compile-time constant after unrolling
+// makes this one v_readlane into a scalar register).
+__device__ __forceinline__ float lane_value(float x, int l) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), l));
 }
 
 __device__ __forceinline__ int uniform_int(int x) {

@@ -29,10 +29,6 @@ namespace w2v {
 
 constexpr int kPairBlock = 8;  // output rows gathered per reduction
 
-__device__ __forceinline__ float lane_value(float x, int l) {
-  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), l));
-}
-
 // Negative k (lane k < K) of input word i of the target at raw position p.
 __device__ __forceinline__ int pair_negative(const EpochArgs& a, int64_t p,
                                              int i, int k) {

@@ -21,8 +21,8 @@
 // range-checked buffer descriptors. Each (input word, output word) pair
 // leaves a per-lane partial dot product; the wave-wide transposing reduction
 // turns up to 64 such partials into one total per lane, the error is
-// evaluated lane-parallel and broadcast through LDS, and the two gradient
-// products are lane-local FMAs.
+// evaluated lane-parallel and read back per slot with v_readlane, and the
+// two gradient products are lane-local FMAs.
 //
 // Update path (live matrices): rows with id < hot_rows receive fp32 atomic
 // adds (frequent words, whose concurrent updates would otherwise overwrite
@@ -59,7 +59,6 @@ struct MinibatchLds {
   int raw[kWave];           // negatives as drawn
   int out[kMaxOutputs];     // [0] target, then distinct unmasked negatives
   float wgt[kMaxOutputs];   // multiplicity of each output column
-  float E[kWave];           // error block of the current output block
 };
 
 // Stages the input rows: the lanes with `present` set hold the input words
@@ -200,6 +199,7 @@ __device__ __forceinline__ void run_minibatch(
   auto read_split = [&](int m, int id, float (&r)[C]) {
     if (id < split_rows) {
       float* pb = part_base(m, id);
+#pragma unroll 1
       for (int g = 0; g < kSplitParts; ++g) {
         float t[C];
         load_row<C, true>(pb, g, ld, D, lane, t);
@@ -257,26 +257,18 @@ __device__ __forceinline__ void run_minibatch(
       }
     }
 
-    // Per-lane partial logits, slot s = i*KB + kk.
-    float v[kWave];
+    // Per-lane partial logits, slot s = i*KB + kk, formed as the reduction
+    // consumes them.
+    auto partial = [&](int s) -> float {
+      const int i = s / KB;
+      const int kk = s % KB;
+      if (s >= kSlots || i >= n) return 0.f;
+      float acc = 0.f;
 #pragma unroll
-    for (int i = 0; i < NMAX; ++i) {
-      if (i < n) {
-#pragma unroll
-        for (int kk = 0; kk < KB; ++kk) {
-          float acc = 0.f;
-#pragma unroll
-          for (int c = 0; c < C; ++c) acc = fmaf(a[i][c], o[kk][c], acc);
-          v[i * KB + kk] = acc;
-        }
-      } else {
-#pragma unroll
-        for (int kk = 0; kk < KB; ++kk) v[i * KB + kk] = 0.f;
-      }
-    }
-#pragma unroll
-    for (int s = kSlots; s < kWave; ++s) v[s] = 0.f;
-    const float x = xpose_reduce64(v, lane);
+      for (int c = 0; c < C; ++c) acc = fmaf(a[i][c], o[kk][c], acc);
+      return acc;
+    };
+    const float x = xpose_reduce64_lazy(partial, lane);
 
     // Error of slot `lane` (input row li, output column lk).
     const int li = lane / KB;
@@ -287,9 +279,10 @@ __device__ __forceinline__ void run_minibatch(
     // negative; evaluating sigma(z) directly avoids cancelling against 1.
     const float z = (lk == 0) ? -x : x;
     const float sz = 1.f / (1.f + __expf(-z));
-    mb.E[lane] = valid ? wgt * alpha * ((lk == 0) ? sz : -sz) : 0.f;
+    // Lane s keeps the error of slot s; the gradient products read it back
+    // with v_readlane (a scalar operand of the FMAs, no LDS round trip).
+    const float e_lane = valid ? wgt * alpha * ((lk == 0) ? sz : -sz) : 0.f;
     if (want_loss && valid) loss_part += wgt * softplus(z);
-    __syncthreads();
 
     // dO = E^T A for the block's output rows.
 #pragma unroll
@@ -302,7 +295,7 @@ __device__ __forceinline__ void run_minibatch(
 #pragma unroll
         for (int i = 0; i < NMAX; ++i) {
           if (i < n) {
-            const float e = mb.E[i * KB + kk];
+            const float e = lane_value(e_lane, i * KB + kk);
 #pragma unroll
             for (int c = 0; c < C; ++c) g[c] = fmaf(e, a[i][c], g[c]);
           }
@@ -320,7 +313,7 @@ __device__ __forceinline__ void run_minibatch(
         for (int c = 0; c < C; ++c) g[c] = kMulti ? ga[kMulti ? i : 0][c] : 0.f;
 #pragma unroll
         for (int kk = 0; kk < KB; ++kk) {
-          const float e = mb.E[i * KB + kk];
+          const float e = lane_value(e_lane, i * KB + kk);
 #pragma unroll
           for (int c = 0; c < C; ++c) g[c] = fmaf(e, o[kk][c], g[c]);
         }
