@@ -2,7 +2,8 @@
 oracle's (the statistical comparison of full runs): the nearest-neighbour
 topic score must agree within one point at every point the oracle's run
 recorded (three points inside epoch 0, where the score climbs from chance to
-0.9, and the end of every epoch). The oracle's scores are stored by
+0.9, and the end of every epoch), and each epoch's mean training loss per
+input word must agree within 2%. The oracle's values are stored by
 tests/golden/make_planted_score.py; a partial file (a run still going)
 compares the points it holds."""
 import json
@@ -38,19 +39,26 @@ def test_planted_topic_recovery_within_one_point():
     thr = torch.from_numpy(thr_h.view(np.int32)).to(dev)
     M_in = w2v.alloc_matrix(planted.V, planted.D, dev, torch.from_numpy(planted.init_in()))
     M_out = w2v.alloc_matrix(planted.V, planted.D, dev)
-    got = {}
+    got, loss = {}, {}
     for e in range(last_epoch + 1):
         cuts = sorted(t for (ee, t) in want if ee == e and t < planted.T)
         bounds = [0] + cuts + [planted.T]
+        lb = torch.zeros((1, 2), dtype=torch.float64, device=dev)
         for lo, hi in zip(bounds[:-1], bounds[1:]):
             # ids are not frequency ranks here, so every row is updated atomically
             w2v.train_epoch(c, M_in, M_out, table, thr, window=planted.WINDOW,
                             K=planted.K, alpha0=planted.ALPHA0, epoch=e,
                             n_epochs=planted.EPOCHS, seed=planted.SAMPLING_SEED,
-                            sentence_len=planted.SENTENCE, pos_begin=lo, pos_end=hi)
+                            sentence_len=planted.SENTENCE, pos_begin=lo, pos_end=hi,
+                            loss_buckets=lb)
             if (e, hi) in want:
                 torch.cuda.synchronize()
                 got[(e, hi)] = planted.nn_topic_score(M_in.cpu().numpy())
+        l = lb.cpu().numpy()
+        loss[e] = l[0, 0] / l[0, 1]
     bad = {k: (got[k], want[k]) for k in want if abs(got[k] - want[k]) > 0.01}
     assert not bad, bad
+    for ep in golden["epochs"]:
+        o = ep["mean_loss_per_input"]
+        assert abs(loss[ep["epoch"]] - o) <= 0.02 * o, (ep["epoch"], loss[ep["epoch"]], o)
     assert max(got.values()) > 0.5                      # far above chance (1%)
