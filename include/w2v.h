@@ -49,7 +49,11 @@ extern "C" {
 #define W2V_ENOMEM (-3)      /* a host allocation failed */
 #define W2V_EUNSUPPORTED (-4)/* valid arguments outside the compiled shapes */
 
-/* Shape limits of the compiled kernels. */
+/* Shape limits of the compiled kernels. The HogBatch kernels keep all N
+ * input rows of a minibatch in registers, so they compile D <= 640 for up to
+ * 10 input words (window <= 5), D <= 320 for up to 16 (window <= 8) and
+ * D <= 128 for up to 32 (window <= 16); other valid combinations return
+ * W2V_EUNSUPPORTED. Algorithm 1 compiles D <= 640 at every window. */
 #define W2V_MAX_DIM 640          /* D */
 #define W2V_MAX_WINDOW 16        /* window: up to 2*window input words */
 #define W2V_MAX_NEGATIVE 64      /* K */

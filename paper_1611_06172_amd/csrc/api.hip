@@ -176,9 +176,11 @@ int w2v_train_epoch(const int32_t* corpus, int64_t T, int64_t pos_begin,
     if (((uintptr_t)workspace & 255u) != 0)
       return fail(W2V_EINVAL, "workspace must be 256-byte aligned");
   }
+  const bool pairwise = algorithm == W2V_ALGORITHM_PAIRWISE;
   const int C = columns_for(D);
   const int nmax = inputs_cap_for(2 * window);
-  if (C == 0 || nmax == 0 || !train_shape_supported(C, nmax))
+  // Algorithm 1 handles one input word at a time: only D limits it.
+  if (C == 0 || nmax == 0 || (!pairwise && !train_shape_supported(C, nmax)))
     return failf(W2V_EUNSUPPORTED, "no compiled kernel for D=%d window=%d", D,
                  window);
   const int64_t n_sent = (pos_end - pos_begin + sentence_len - 1) / sentence_len;
@@ -213,7 +215,6 @@ int w2v_train_epoch(const int32_t* corpus, int64_t T, int64_t pos_begin,
   a.split_rows = split_rows;
   a.part = (float*)workspace;
 
-  const bool pairwise = algorithm == W2V_ALGORITHM_PAIRWISE;
   int64_t grid = max_inflight;
   if (grid == 0) {
     const int per_cu = pairwise ? pairwise_blocks_per_cu(C, K)
