@@ -86,6 +86,11 @@ def lib():
                                                   _f32p, ctypes.c_int32, ctypes.c_int32,
                                                   ctypes.c_int32, _f64p, ctypes.c_int32]
         L.oracle_pairwise_train_epoch.restype = ctypes.c_int64
+        L.oracle_grouped_train_epoch.argtypes = [ctypes.POINTER(_Sampling), ctypes.c_int32,
+                                                 _f32p, _f32p, ctypes.c_int32,
+                                                 ctypes.c_int32, ctypes.c_int32, _f64p,
+                                                 ctypes.c_int32]
+        L.oracle_grouped_train_epoch.restype = ctypes.c_int64
         _lib = L
     return _lib
 
@@ -319,4 +324,21 @@ def pairwise_train_epoch(s: Sampling, M_in, M_out, D=None, n_buckets=0):
                                           _ptr(buckets, _f64p), n_buckets)
     if n < 0:
         raise ValueError("oracle_pairwise_train_epoch failed")
+    return n, buckets
+
+
+def grouped_train_epoch(s: Sampling, G: int, M_in, M_out, D=None, n_buckets=0):
+    """HogBatch with negatives shared by groups of G consecutive targets,
+    sequential, in place. Returns (minibatches applied, loss buckets)."""
+    assert M_in.dtype == np.float32 and M_in.flags.c_contiguous
+    assert M_out.dtype == np.float32 and M_out.flags.c_contiguous
+    V, ld = M_in.shape
+    D = ld if D is None else D
+    st = s._struct()
+    buckets = np.zeros((n_buckets, 2)) if n_buckets > 0 else None
+    n = lib().oracle_grouped_train_epoch(ctypes.byref(st), G, _ptr(M_in, _f32p),
+                                         _ptr(M_out, _f32p), V, D, ld,
+                                         _ptr(buckets, _f64p), n_buckets)
+    if n < 0:
+        raise ValueError("oracle_grouped_train_epoch failed")
     return n, buckets

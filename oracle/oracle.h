@@ -148,6 +148,18 @@ int64_t oracle_pairwise_train_epoch(const oracle_sampling* s, float* M_in,
                                     int32_t ld, double* loss_buckets,
                                     int32_t n_buckets);
 
+/* HogBatch with the K negatives shared by the G consecutive targets of a
+ * group (retained indices [q0, q0+G), q0 a multiple of G, within a
+ * sentence): negatives drawn at the group's first retained position, every
+ * member's step from the rows as they were before the group, all updates
+ * summed per row and rounded once. G = 1 is oracle_train_epoch. Returns the
+ * number of minibatches (members) applied. A group's loss goes to the bucket
+ * of its first member. */
+int64_t oracle_grouped_train_epoch(const oracle_sampling* s, int32_t G,
+                                   float* M_in, float* M_out, int32_t V,
+                                   int32_t D, int32_t ld, double* loss_buckets,
+                                   int32_t n_buckets);
+
 #ifdef __cplusplus
 }
 #endif

@@ -422,3 +422,114 @@ int64_t oracle_pairwise_train_epoch(const oracle_sampling* s, float* M_in,
   oracle_sentence_free(&sen);
   return status == 0 ? applied : status;
 }
+
+/*
+ * Negatives shared across a group of consecutive targets (a generalisation
+ * of the sharing across one target's input words, Sec. 1.1). Reading: the
+ * retained targets of a sentence are cut into groups of G consecutive
+ * retained indices (q0 = 0, G, 2G, ...); the members of a group are those
+ * that form a minibatch; all members take the K negatives drawn at the
+ * group's first retained position (draws 2..K+1 of its stream; a negative
+ * equal to a member's own target is masked for that member only). Every
+ * member's minibatch step is computed from the rows as they were before the
+ * group, and the updates of all members are summed per row in fp64 and
+ * rounded once when the group ends. With G = 1 this is the HogBatch epoch.
+ * The loss of a group is credited to the bucket of its first member.
+ */
+int64_t oracle_grouped_train_epoch(const oracle_sampling* s, int32_t G,
+                                   float* M_in, float* M_out, int32_t V,
+                                   int32_t D, int32_t ld, double* loss_buckets,
+                                   int32_t n_buckets) {
+  if (oracle_validate_sampling(s) != 0 || G < 1) return -1;
+  if (M_in == NULL || M_out == NULL || V <= 0 || D <= 0 || ld < D) return -1;
+  if (loss_buckets != NULL && n_buckets <= 0) return -1;
+  oracle_sentence sen;
+  if (oracle_sentence_alloc(&sen, s->sentence_len, s->window, s->K) != 0)
+    return -2;
+  const int32_t w2 = 2 * s->window;
+  const int32_t K = s->K;
+  const int32_t C = K + 1;
+  /* all members' snapshot rows and deltas, one after another */
+  double* A = (double*)malloc(sizeof(double) * (size_t)G * w2 * D);
+  double* O = (double*)malloc(sizeof(double) * (size_t)G * C * D);
+  double* dA = (double*)malloc(sizeof(double) * (size_t)G * w2 * D);
+  double* dO = (double*)malloc(sizeof(double) * (size_t)G * C * D);
+  double* acc = (double*)malloc(sizeof(double) * (size_t)D);
+  int32_t* rows_in = (int32_t*)malloc(sizeof(int32_t) * (size_t)G * w2);
+  int32_t* rows_out = (int32_t*)malloc(sizeof(int32_t) * (size_t)G * C);
+  int32_t* negs = (int32_t*)malloc(sizeof(int32_t) * (size_t)(K + 1));
+  uint8_t* mask = (uint8_t*)malloc((size_t)(K + 1));
+  int32_t* q_of = (int32_t*)malloc(sizeof(int32_t) * (size_t)s->sentence_len);
+  int status = (A && O && dA && dO && acc && rows_in && rows_out && negs &&
+                mask && q_of) ? 0 : -2;
+  int64_t applied = 0;
+  for (int64_t sb = s->pos_begin; sb < s->pos_end && status == 0;
+       sb += s->sentence_len) {
+    int64_t se = sb + s->sentence_len;
+    if (se > s->T) se = s->T;
+    int32_t n_mb = oracle_sentence_minibatches(s, sb, se, &sen);
+    /* retained index of every minibatch's target */
+    for (int32_t m = 0, q = 0; m < n_mb; ++m) {
+      while (sen.ret_pos[q] != sen.pos[m]) ++q;
+      q_of[m] = q;
+    }
+    for (int32_t m0 = 0; m0 < n_mb && status == 0;) {
+      const int32_t q0 = q_of[m0] - q_of[m0] % G;
+      int32_t n_mem = 0;
+      while (m0 + n_mem < n_mb && q_of[m0 + n_mem] < q0 + G) ++n_mem;
+      /* the group's negatives: draws at its first retained position */
+      const int64_t p0 = sen.ret_pos[q0];
+      for (int32_t k = 0; k < K; ++k) {
+        uint32_t r = oracle_draw_u32(s->seed, (uint64_t)p0, (uint64_t)s->epoch,
+                                     2u + (uint32_t)k);
+        negs[k] = s->neg_table[((uint64_t)r * (uint64_t)s->table_size) >> 32];
+        if (negs[k] < 0 || negs[k] >= V) status = -1;
+      }
+      if (status != 0) break;
+      double loss = 0.0;
+      int32_t n_in = 0;  /* input rows of all members so far */
+      for (int32_t g = 0; g < n_mem; ++g) {
+        const int32_t m = m0 + g;
+        const int32_t n = sen.n_ctx[m];
+        const int32_t* ctx = sen.ctx + (size_t)m * w2;
+        for (int32_t i = 0; i < n; ++i) {
+          if (ctx[i] < 0 || ctx[i] >= V) status = -1;
+          rows_in[n_in + i] = ctx[i];
+        }
+        if (status != 0) break;
+        for (int32_t i = 0; i < n; ++i)
+          for (int32_t j = 0; j < D; ++j)
+            A[((size_t)n_in + i) * D + j] = (double)M_in[(size_t)ctx[i] * ld + j];
+        for (int32_t k = 0; k <= K; ++k) {
+          const int32_t id = k == 0 ? sen.target[m] : negs[k - 1];
+          rows_out[g * C + k] = id;
+          for (int32_t j = 0; j < D; ++j)
+            O[((size_t)g * C + k) * D + j] = (double)M_out[(size_t)id * ld + j];
+        }
+        for (int32_t k = 0; k < K; ++k) mask[k] = (uint8_t)(negs[k] == sen.target[m]);
+        double l = 0.0;
+        oracle_sgns_delta(n, K, D, A + (size_t)n_in * D, O + (size_t)g * C * D,
+                          mask, (double)sen.alpha[m], NULL, dA + (size_t)n_in * D,
+                          dO + (size_t)g * C * D, &l);
+        loss += l;
+        n_in += n;
+      }
+      if (status != 0) break;
+      /* every member read the rows as they were before the group; the sums
+       * per row are rounded once */
+      write_back(M_in, D, ld, n_in, rows_in, dA, acc);
+      write_back(M_out, D, ld, n_mem * C, rows_out, dO, acc);
+      if (loss_buckets != NULL) {
+        int64_t b = sen.pos[m0] * (int64_t)n_buckets / s->T;
+        loss_buckets[2 * b] += loss;
+        loss_buckets[2 * b + 1] += (double)n_in;
+      }
+      applied += n_mem;
+      m0 += n_mem;
+    }
+  }
+  free(A); free(O); free(dA); free(dO); free(acc); free(rows_in); free(rows_out);
+  free(negs); free(mask); free(q_of);
+  oracle_sentence_free(&sen);
+  return status == 0 ? applied : status;
+}
