@@ -60,6 +60,9 @@ def main():
     ap.add_argument("--window", type=int, default=5)
     ap.add_argument("--sample", type=float, default=1e-4)
     ap.add_argument("--max-inflight", type=int, default=0)
+    ap.add_argument("--group", type=int, default=1,
+                    help="consecutive targets sharing one draw of negatives "
+                         "(1: HogBatch as in the paper)")
     ap.add_argument("--algorithm", choices=["hogbatch", "pairwise"], default="hogbatch",
                     help="hogbatch (Sec. 1.1, the measured path) or pairwise "
                          "(Alg. 1, the paper's baseline, for comparison)")
@@ -138,7 +141,7 @@ def main():
                         n_epochs=n_epochs, seed=1234, sentence_len=L,
                         stats=stats, max_inflight=args.max_inflight,
                         hot_rows=hot, split_rows=split, workspace=workspace,
-                        algorithm=args.algorithm)
+                        algorithm=args.algorithm, group=args.group)
 
     for i in range(args.warmup):
         step(i)
@@ -176,7 +179,7 @@ def main():
     avg_kern_s = float(np.mean(kern_ms)) / 1e3
     achieved = alg_bytes / avg_kern_s / 1e9
     traffic = (measured_traffic(args.traffic_json, 1.0)
-               if args.algorithm == "hogbatch" else None)
+               if args.algorithm == "hogbatch" and args.group == 1 else None)
 
     result = {
         "metric": METRIC,
@@ -197,6 +200,7 @@ def main():
                          f"T={T}, V={V}, D={D}, K={K}, window={W}, sample={args.sample}, "
                          f"sentence {L}, alpha 0.025 linear"),
             "V": V, "T": T, "D": D, "ld": ld, "K": K, "window": W, "sample": args.sample,
+            "group": args.group,
             "inflight_sentences": int(inflight), "atomic_rows": int(hot),
             "split_rows": int(split),
             "minibatches_per_step": int(n_mb), "mean_inputs_per_minibatch":

@@ -155,6 +155,17 @@ int64_t w2v_default_inflight(int32_t D, int32_t window, int32_t K);
  * that row moves right after its pair, and the M_in row of i moves once,
  * after its K+1 pairs. A target with any negative outside [0, V) is skipped
  * and counted in stats[3]. split_rows must be 0 with this algorithm.
+ * group (HogBatch only; 1 is the paper's method): G in {2, 4, 8} shares the
+ * K negatives among G consecutive targets instead of one target's input
+ * words (the sharing of Sec. 1.1 widened). The retained targets of a
+ * sentence are cut at multiples of G; the members of a group (its targets
+ * with input words) take the negatives drawn at the group's first retained
+ * position (draws 2..K+1 of its stream); a negative equal to a member's own
+ * target is masked for that member; all members' steps read the rows as
+ * they were before the group and their updates to a row are summed; a
+ * group's loss goes to the bucket of its first member. Needs 2 window G <=
+ * 64 and G + K <= 64; the positions a group's windows span (2 window + G)
+ * must fit a compiled input capacity (10, 16 or 32, see the shape limits).
  * Update path: a row with id < hot_rows receives fp32 atomic adds (no update
  * is lost under concurrency); a row with id >= hot_rows is written back as
  * (value read + update) by a store written through to device scope, so a
@@ -201,7 +212,8 @@ int w2v_train_epoch(const int32_t* corpus, int64_t T, int64_t pos_begin,
                     int32_t n_epochs, uint64_t seed, double* loss_buckets,
                     int32_t n_buckets, int64_t* stats, int32_t max_inflight,
                     int32_t hot_rows, int32_t split_rows, void* workspace,
-                    size_t workspace_bytes, int32_t algorithm, void* stream);
+                    size_t workspace_bytes, int32_t algorithm, int32_t group,
+                    void* stream);
 
 /* Workspace bytes w2v_train_epoch needs for split_rows rows of stride ld:
  * 2 * split_rows * W2V_SPLIT_PARTS * ld * 4 (0 when split_rows is 0). */

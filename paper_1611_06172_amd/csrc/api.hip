@@ -153,7 +153,8 @@ int w2v_train_epoch(const int32_t* corpus, int64_t T, int64_t pos_begin,
                     int32_t n_epochs, uint64_t seed, double* loss_buckets,
                     int32_t n_buckets, int64_t* stats, int32_t max_inflight,
                     int32_t hot_rows, int32_t split_rows, void* workspace,
-                    size_t workspace_bytes, int32_t algorithm, void* stream) {
+                    size_t workspace_bytes, int32_t algorithm, int32_t group,
+                    void* stream) {
   int rc = check_sampling({corpus, T, pos_begin, pos_end, sentence_len, V,
                            window, K, neg_table, table_size, epoch, n_epochs});
   if (rc != W2V_OK) return rc;
@@ -169,6 +170,12 @@ int w2v_train_epoch(const int32_t* corpus, int64_t T, int64_t pos_begin,
     return fail(W2V_EINVAL, "split_rows must be in [0, V]");
   if (algorithm == W2V_ALGORITHM_PAIRWISE && split_rows != 0)
     return fail(W2V_EINVAL, "split_rows must be 0 with the pairwise algorithm");
+  if (group != 1 && group != 2 && group != 4 && group != 8)
+    return fail(W2V_EINVAL, "group must be 1, 2, 4 or 8");
+  if (group > 1 && algorithm != W2V_ALGORITHM_HOGBATCH)
+    return fail(W2V_EINVAL, "group > 1 needs the HogBatch algorithm");
+  if (group > 1 && (group * 2 * window > 64 || group + K > 64))
+    return fail(W2V_EINVAL, "group needs 2 * window * group <= 64 and group + K <= 64");
   if (split_rows > 0) {
     if (workspace == nullptr) return fail(W2V_EINVAL, "workspace is NULL");
     if (workspace_bytes < w2v_train_epoch_workspace_bytes(split_rows, ld))
@@ -177,8 +184,11 @@ int w2v_train_epoch(const int32_t* corpus, int64_t T, int64_t pos_begin,
       return fail(W2V_EINVAL, "workspace must be 256-byte aligned");
   }
   const bool pairwise = algorithm == W2V_ALGORITHM_PAIRWISE;
+  const bool grouped = group > 1;
   const int C = columns_for(D);
-  const int nmax = inputs_cap_for(2 * window);
+  // distinct input rows of a group: at most the 2 window + group positions
+  // its members' windows span (2 window for one target)
+  const int nmax = inputs_cap_for(grouped ? 2 * window + group : 2 * window);
   // Algorithm 1 handles one input word at a time: only D limits it.
   if (C == 0 || nmax == 0 || (!pairwise && !train_shape_supported(C, nmax)))
     return failf(W2V_EUNSUPPORTED, "no compiled kernel for D=%d window=%d", D,
@@ -214,11 +224,13 @@ int w2v_train_epoch(const int32_t* corpus, int64_t T, int64_t pos_begin,
   a.hot_rows = hot_rows;
   a.split_rows = split_rows;
   a.part = (float*)workspace;
+  a.group = group;
 
   int64_t grid = max_inflight;
   if (grid == 0) {
-    const int per_cu = pairwise ? pairwise_blocks_per_cu(C, K)
-                                : epoch_blocks_per_cu(C, nmax, window, K);
+    const int per_cu = pairwise  ? pairwise_blocks_per_cu(C, K)
+                       : grouped ? grouped_blocks_per_cu(C, nmax, K)
+                                 : epoch_blocks_per_cu(C, nmax, window, K);
     const int cus = cu_count();
     grid = (int64_t)(per_cu > 0 ? per_cu : 1) * (cus > 0 ? cus : 1);
   }
@@ -230,8 +242,9 @@ int w2v_train_epoch(const int32_t* corpus, int64_t T, int64_t pos_begin,
     e = launch_part_clear(a, s);
     if (e != hipSuccess) return hip_fail(e, "partial-row clear launch");
   }
-  e = pairwise ? launch_pairwise(C, a, (int)grid, s)
-               : launch_train(C, nmax, a, (int)grid, s);
+  e = pairwise  ? launch_pairwise(C, a, (int)grid, s)
+      : grouped ? launch_grouped(C, nmax, a, (int)grid, s)
+                : launch_train(C, nmax, a, (int)grid, s);
   if (e != hipSuccess) return hip_fail(e, "train kernel launch");
   if (split_rows > 0) {
     e = launch_part_fold(a, s);

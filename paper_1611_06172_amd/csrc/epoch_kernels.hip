@@ -11,6 +11,7 @@
 // It serves every compiled shape, including output blocks that take several
 // reductions. The export variant stops after step 2 and writes the
 // minibatches out.
+#include "group_core.h"
 #include "kernel_args.h"
 #include "sentence.h"
 #include "sgns_core.h"
@@ -116,6 +117,154 @@ __global__ __launch_bounds__(256) void k_part_fold(EpochArgs a) {
   }
 }
 
+// The same epoch with the K negatives shared by groups of G consecutive
+// targets (group_core.h): per group, the members' input occurrences and the
+// output candidates (member targets, then the group's negatives) are staged
+// deduplicated with their group tables, then one snapshot step runs over the
+// group. Groups start at retained indices that are multiples of G (G divides
+// the 64-target batches).
+template <int C, int NMAX>
+__global__ __launch_bounds__(kWave) void k_epoch_grouped(EpochArgs a) {
+  __shared__ SentenceLds sl;
+  __shared__ TargetBatch tb;
+  __shared__ MinibatchLds mb;
+  __shared__ GroupLds gl;
+  extern __shared__ int32_t negs_lds[];  // [kWave][K]
+  const int lane = threadIdx.x;
+  const int K = a.K;
+  const int G = a.group;
+  const bool want_loss = a.loss != nullptr;
+
+  int64_t n_mb = 0, sum_n = 0, raw = 0, rejected = 0;
+  double lsum = 0.0, lcnt = 0.0;
+  int bucket = -1;
+
+  for (int64_t s = blockIdx.x; s < a.n_sent; s += gridDim.x) {
+    const int64_t sb = a.pos_begin + s * a.L;
+    const int64_t se = min(sb + (int64_t)a.L, a.pos_end);
+    const int len = (int)(se - sb);
+    raw += len;
+    const int n_ret = keep_and_compact<false>(a, sb, len, lane, sl, rejected);
+
+    for (int q0 = 0; q0 < n_ret; q0 += kWave) {
+      form_targets<false>(a, sb, q0, n_ret, lane, sl, tb, negs_lds);
+      const int cnt = min(kWave, n_ret - q0);
+      for (int j0 = 0; j0 < cnt; j0 += G) {
+        // Members: lane g < G holds the input count of target j0 + g.
+        const int n_g = (lane < G && j0 + lane < cnt) ? tb.n[j0 + lane] : 0;
+        const uint64_t members = __ballot(n_g > 0);
+        if (members == 0ull) continue;
+        if (uniform_int(tb.bad[j0]) != 0) {
+          rejected += __popcll(members);
+          continue;
+        }
+        // Input occurrences, member by member, one per lane.
+        int off = 0, my_g = -1, my_i = 0;
+#pragma unroll
+        for (int g = 0; g < kMaxGroup; ++g) {
+          if (g < G) {
+            const int ng = __builtin_amdgcn_readlane(n_g, g);
+            if (lane >= off && lane < off + ng) {
+              my_g = g;
+              my_i = lane - off;
+            }
+            off += ng;
+          }
+        }
+        const int total = off;
+        if (my_g >= 0) {
+          const int q = q0 + j0 + my_g;
+          int jj = tb.lo[j0 + my_g] + my_i;
+          if (jj >= q) ++jj;
+          gl.occ_id[lane] = sl.ret_id[jj];
+          gl.occ_g[lane] = my_g;
+        }
+        if (lane < G)
+          gl.alpha[lane] = n_g > 0 ? tb.alpha[j0 + lane] : 0.f;
+        // Output candidates: member targets, then the group's negatives
+        // (drawn at its first retained position).
+        int cid = -1;
+        if (lane < G) {
+          if (n_g > 0) cid = sl.ret_id[q0 + j0 + lane];
+        } else if (lane < G + K) {
+          cid = negs_lds[j0 * K + (lane - G)];
+        }
+        gl.cand_id[lane] = cid;
+        __syncthreads();
+
+        // Distinct input rows and their multiplicity per member.
+        const int my_id = my_g >= 0 ? gl.occ_id[lane] : -1;
+        bool first = my_g >= 0;
+        float mult[kMaxGroup];
+#pragma unroll
+        for (int g = 0; g < kMaxGroup; ++g) mult[g] = 0.f;
+        if (my_g >= 0) {
+          for (int l2 = 0; l2 < total; ++l2) {
+            if (gl.occ_id[l2] != my_id) continue;
+            if (l2 < lane) first = false;
+            const int g2 = gl.occ_g[l2];
+#pragma unroll
+            for (int g = 0; g < kMaxGroup; ++g) mult[g] += (g2 == g) ? 1.f : 0.f;
+          }
+        }
+        const uint64_t fin = __ballot(first);
+        if (first) {
+          const int dst = __popcll(fin & lanes_below(lane));
+          mb.ctx[dst] = my_id;
+#pragma unroll
+          for (int g = 0; g < kMaxGroup; ++g) gl.m[dst][g] = mult[g];
+        }
+        const int n_in = __popcll(fin);
+
+        // Distinct output columns: member-target bits and negative weight.
+        bool cfirst = cid >= 0;
+        uint32_t bits = 0u;
+        float nw = 0.f;
+        if (cid >= 0) {
+          for (int c2 = 0; c2 < G + K; ++c2) {
+            if (gl.cand_id[c2] != cid) continue;
+            if (c2 < lane) cfirst = false;
+            if (c2 < G) bits |= 1u << c2;
+            else nw += 1.f;
+          }
+        }
+        const uint64_t fout = __ballot(cfirst);
+        if (cfirst) {
+          const int dst = __popcll(fout & lanes_below(lane));
+          mb.out[dst] = cid;
+          gl.tbits[dst] = bits;
+          gl.negw[dst] = nw;
+        }
+        const int n_out = __popcll(fout);
+        __syncthreads();
+
+        n_mb += __popcll(members);
+        sum_n += total;
+        float loss_part = 0.f;
+        run_minibatch<C, NMAX, true, true, false, GroupError>(
+            a.M_in, a.M_out, a.M_in, a.M_out, a.ld, a.D, lane, n_in, n_out, 0.f,
+            a.hot_rows, mb, want_loss, loss_part, a.part, a.split_rows,
+            GroupError{&gl, G});
+        if (want_loss) {
+          const int qf = q0 + j0 + (int)__builtin_ctzll(members);
+          const int64_t p = sb + sl.ret_off[qf];
+          const int b = (int)(p * (int64_t)a.n_buckets / a.T);
+          if (b != bucket) {
+            if (bucket >= 0) flush_loss(a.loss, bucket, lsum, lcnt, lane);
+            bucket = b;
+          }
+          lsum += (double)loss_part;
+          if (lane == 0) lcnt += (double)total;
+        }
+        __syncthreads();
+      }
+      __syncthreads();
+    }
+  }
+  if (want_loss && bucket >= 0) flush_loss(a.loss, bucket, lsum, lcnt, lane);
+  flush_stats(a.stats, lane, n_mb, sum_n, raw, rejected);
+}
+
 // ------------------------------------------------------------ launchers --
 
 static int part_grid(int64_t n) {
@@ -190,6 +339,33 @@ int train_blocks_per_cu(int C, int nmax, int K) {
 hipError_t launch_train(int C, int nmax, const EpochArgs& a, int grid,
                         hipStream_t s) {
   EpochKernel k = train_kernel_for(C, nmax, a.K);
+  if (k == nullptr) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k, dim3(grid), dim3(kWave), epoch_dyn_lds(a), s, a);
+  return hipGetLastError();
+}
+
+static EpochKernel grouped_kernel_for(int C, int nmax) {
+#define W2V_PICK(c, n) \
+  if (C == c && nmax == n) return k_epoch_grouped<c, n>;
+  W2V_TRAIN_SHAPES(W2V_PICK)
+#undef W2V_PICK
+  return nullptr;
+}
+
+int grouped_blocks_per_cu(int C, int nmax, int K) {
+  EpochKernel k = grouped_kernel_for(C, nmax);
+  if (k == nullptr) return 0;
+  int blocks = 0;
+  const size_t dyn = sizeof(int32_t) * kWave * (size_t)(K > 0 ? K : 1);
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, k, kWave, dyn) !=
+      hipSuccess)
+    return 0;
+  return blocks;
+}
+
+hipError_t launch_grouped(int C, int nmax, const EpochArgs& a, int grid,
+                          hipStream_t s) {
+  EpochKernel k = grouped_kernel_for(C, nmax);
   if (k == nullptr) return hipErrorInvalidValue;
   hipLaunchKernelGGL(k, dim3(grid), dim3(kWave), epoch_dyn_lds(a), s, a);
   return hipGetLastError();

@@ -28,6 +28,7 @@ struct EpochArgs {
   int64_t* stats;          // NULL or int64[4]
   int32_t hot_rows;        // ids below this get atomic updates
   int32_t split_rows;      // ids below this use partial rows in `part`
+  int32_t group;           // consecutive targets sharing one negative draw
   float* part;             // [2][split_rows][kSplitParts][ld] partial rows
   // export outputs (minibatch export only)
   int32_t* out_targets;
@@ -68,6 +69,10 @@ bool train_shape_supported(int C, int nmax);
 int columns_for(int D);      // compiled C for a row length, 0 if none
 int inputs_cap_for(int n);   // compiled nmax for n input words, 0 if none
 int train_blocks_per_cu(int C, int nmax, int K);
+// HogBatch with negatives shared by groups of targets (any K: multi-block).
+int grouped_blocks_per_cu(int C, int nmax, int K);
+hipError_t launch_grouped(int C, int nmax, const EpochArgs& a, int grid,
+                          hipStream_t s);
 // Algorithm 1 (per-pair) epoch kernel.
 int pairwise_blocks_per_cu(int C, int K);
 hipError_t launch_pairwise(int C, const EpochArgs& a, int grid, hipStream_t s);

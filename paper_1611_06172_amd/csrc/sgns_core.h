@@ -178,20 +178,39 @@ __device__ __forceinline__ float softplus(float z) {
   return fmaxf(z, 0.f) + log1pf(__expf(-fabsf(z)));
 }
 
+// Error and loss of slot (input row li, output column lk) of a minibatch of
+// one target: column 0 is the target (label 1), the others negatives
+// (label 0); both scaled by the row and column multiplicities.
+struct TargetError {
+  __device__ __forceinline__ float operator()(const MinibatchLds& mb, int li,
+                                              int lk, float x, float alpha,
+                                              bool want_loss,
+                                              float& loss_part) const {
+    const float wgt = mb.wgt[lk] * mb.cwgt[li];
+    // label - sigma(x) is sigma(-x) for the target and -sigma(x) for a
+    // negative; evaluating sigma(z) directly avoids cancelling against 1.
+    const float z = (lk == 0) ? -x : x;
+    const float sz = 1.f / (1.f + __expf(-z));
+    if (want_loss) loss_part += wgt * softplus(z);
+    return wgt * alpha * ((lk == 0) ? sz : -sz);
+  }
+};
+
 // Runs one minibatch. Rin/Rout: where rows are read; Win/Wout: where updates
 // go (the same fp32 matrices, or fp64 delta buffers with the same row stride
 // when kAccum64). n distinct input rows (n <= NMAX) in mb.ctx/mb.cwgt, n_out
 // distinct output columns in mb.out/mb.wgt. Rows id < split_rows of matrix m
 // (0: input, 1: output) have partial rows part[((m split_rows + id)
-// kSplitParts + g) ld], g < kSplitParts (live matrices only). Every lane
-// returns its share of the minibatch loss in `loss_part` when want_loss is
-// set.
-template <int C, int NMAX, bool kMulti, bool kLiveRead, bool kAccum64>
+// kSplitParts + g) ld], g < kSplitParts (live matrices only). `err` gives
+// the error of a slot (TargetError for one target). Every lane returns its
+// share of the minibatch loss in `loss_part` when want_loss is set.
+template <int C, int NMAX, bool kMulti, bool kLiveRead, bool kAccum64,
+          class Err = TargetError>
 __device__ __forceinline__ void run_minibatch(
     const float* Rin, const float* Rout, void* Win, void* Wout, int64_t ld,
     int D, int lane, int n, int n_out, float alpha, int hot_rows,
     MinibatchLds& mb, bool want_loss, float& loss_part,
-    float* part = nullptr, int split_rows = 0) {
+    float* part = nullptr, int split_rows = 0, const Err& err = Err()) {
   auto part_base = [&](int m, int id) -> float* {
     return part + (int64_t)(m * split_rows + id) * kSplitParts * ld;
   };
@@ -274,15 +293,10 @@ __device__ __forceinline__ void run_minibatch(
     const int li = lane / KB;
     const int lk = k0 + lane % KB;
     const bool valid = lane < kSlots && li < n && lk < n_out;
-    const float wgt = valid ? mb.wgt[lk] * mb.cwgt[li] : 0.f;
-    // label - sigma(x) is sigma(-x) for the target and -sigma(x) for a
-    // negative; evaluating sigma(z) directly avoids cancelling against 1.
-    const float z = (lk == 0) ? -x : x;
-    const float sz = 1.f / (1.f + __expf(-z));
     // Lane s keeps the error of slot s; the gradient products read it back
     // with v_readlane (a scalar operand of the FMAs, no LDS round trip).
-    const float e_lane = valid ? wgt * alpha * ((lk == 0) ? sz : -sz) : 0.f;
-    if (want_loss && valid) loss_part += wgt * softplus(z);
+    float e_lane = 0.f;
+    if (valid) e_lane = err(mb, li, lk, x, alpha, want_loss, loss_part);
 
     // dO = E^T A for the block's output rows.
 #pragma unroll

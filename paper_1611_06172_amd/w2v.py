@@ -56,7 +56,7 @@ def lib():
     L.w2v_train_epoch.argtypes = [
         _vp, _i64, _i64, _i64, _i32, _vp, _vp, _i32, _i32, _i32, _i32, _i32,
         _vp, _i64, _vp, _f32, _f32, _i32, _i32, _u64, _vp, _i32, _vp, _i32, _i32,
-        _i32, _vp, ctypes.c_size_t, _i32, _vp]
+        _i32, _vp, ctypes.c_size_t, _i32, _i32, _vp]
     L.w2v_train_epoch.restype = ctypes.c_int
     L.w2v_train_epoch_workspace_bytes.argtypes = [_i32, _i32]
     L.w2v_train_epoch_workspace_bytes.restype = ctypes.c_size_t
@@ -171,7 +171,7 @@ def train_epoch(corpus, M_in, M_out, neg_table, keep_thresh=None, *,
                 sentence_len: int = 1000, loss_buckets=None, stats=None,
                 max_inflight: int = 0, hot_rows: Optional[int] = None,
                 split_rows: int = 0, workspace=None, algorithm: str = "hogbatch",
-                stream=None):
+                group: int = 1, stream=None):
     """Hogwild HogBatch epoch over corpus[pos_begin:pos_end], in place.
 
     hot_rows: ids below it are updated with atomic adds, the others with
@@ -179,7 +179,9 @@ def train_epoch(corpus, M_in, M_out, neg_table, keep_thresh=None, *,
     split_rows: ids below it are updated through per-XCD partial rows that
     every read sums (see w2v_train_epoch); workspace (a device byte tensor of
     train_epoch_workspace_bytes(split_rows, ld)) is allocated when None.
-    algorithm: "hogbatch" (Sec. 1.1) or "pairwise" (Alg. 1, the baseline)."""
+    algorithm: "hogbatch" (Sec. 1.1) or "pairwise" (Alg. 1, the baseline).
+    group: consecutive targets sharing one draw of negatives (1: HogBatch as
+    in the paper; 2, 4, 8: the sharing widened across targets)."""
     import torch
     _dev(corpus, torch.int32, "corpus", 1)
     V, ld = _matrix(M_in, "M_in")
@@ -213,7 +215,8 @@ def train_epoch(corpus, M_in, M_out, neg_table, keep_thresh=None, *,
         _ptr(keep_thresh), alpha0, min_alpha_frac, epoch, n_epochs, seed,
         _ptr(loss_buckets), n_b, _ptr(stats), max_inflight,
         V if hot_rows is None else int(hot_rows), int(split_rows),
-        _ptr(workspace), ws_bytes, ALGORITHMS[algorithm], _stream(stream)))
+        _ptr(workspace), ws_bytes, ALGORITHMS[algorithm], int(group),
+        _stream(stream)))
 
 
 def padded_ld(D: int) -> int:

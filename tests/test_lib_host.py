@@ -75,7 +75,7 @@ def train(**over):
                 M_out=FAKE, V=10, D=8, ld=8, window=5, K=5, table=FAKE,
                 table_size=100, thr=None, alpha0=0.025, minf=1e-4, epoch=0,
                 n_epochs=1, seed=0, loss=None, n_b=0, stats=None, inflight=0,
-                hot=0, split=0, ws=None, ws_bytes=0, algorithm=0, stream=None)
+                hot=0, split=0, ws=None, ws_bytes=0, algorithm=0, group=1, stream=None)
     args.update(over)
     return w2v.lib().w2v_train_epoch(*args.values())
 
@@ -96,6 +96,9 @@ def train(**over):
     (dict(split=2, ws=0x100010, ws_bytes=1 << 20), "aligned"),
     (dict(algorithm=2), "algorithm"), (dict(algorithm=-1), "algorithm"),
     (dict(algorithm=1, split=1, ws=0x100000, ws_bytes=1 << 20), "pairwise"),
+    (dict(group=3), "group"), (dict(group=0), "group"), (dict(group=16), "group"),
+    (dict(group=2, algorithm=1), "group"), (dict(group=8, window=5), "group"),
+    (dict(group=8, window=2, K=60), "group"),
 ])
 def test_train_epoch_rejects(over, needle):
     assert train(**over) == w2v.EINVAL
