@@ -220,6 +220,31 @@ int w2v_train_epoch(const int32_t* corpus, int64_t T, int64_t pos_begin,
 size_t w2v_train_epoch_workspace_bytes(int32_t split_rows, int32_t ld);
 
 /*
+ * Vocabulary of a raw id stream (GPU; the step before w2v_build_tables: the
+ * paper's corpus is counted and its words ranked, Sec. 2). Counts every id
+ * of raw[0..T) in [0, V_raw) (other values are not counted), ranks the ids
+ * by count, descending, ties by increasing raw id, and keeps the words with
+ * count >= max(min_count, 1).
+ *   ranked_counts device int64[V_raw]: count of the word of rank r for
+ *                 r < V, 0 after (the counts argument of w2v_build_tables);
+ *   rank_of       device int32[V_raw]: the new id of raw id x (its rank), or
+ *                 -1 when x is dropped;
+ *   v_kept        device int32[1]: V, the number of words kept;
+ *   corpus_out    device int32[T] or NULL: raw rewritten in new ids, -1 for
+ *                 dropped words and ids outside [0, V_raw) (the epoch skips
+ *                 such positions before forming windows).
+ * With ids ranked this way id 0 is the most frequent word, as the update
+ * tiers of w2v_train_epoch assume. workspace: device, 256-byte aligned,
+ * >= w2v_build_vocab_workspace_bytes(V_raw) bytes, caller-owned. The call
+ * is asynchronous on `stream`.
+ */
+size_t w2v_build_vocab_workspace_bytes(int32_t V_raw);
+int w2v_build_vocab(const int32_t* raw, int64_t T, int32_t V_raw,
+                    int64_t min_count, int64_t* ranked_counts,
+                    int32_t* rank_of, int32_t* v_kept, int32_t* corpus_out,
+                    void* workspace, size_t workspace_bytes, void* stream);
+
+/*
  * The minibatches w2v_train_epoch would form over [pos_begin, pos_end),
  * written out instead of applied (same arguments and readings as
  * w2v_train_epoch; the matrices are not needed). Outputs are indexed by raw

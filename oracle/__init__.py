@@ -342,3 +342,6 @@ def grouped_train_epoch(s: Sampling, G: int, M_in, M_out, D=None, n_buckets=0):
     if n < 0:
         raise ValueError("oracle_grouped_train_epoch failed")
     return n, buckets
+
+
+from .vocab import build_vocab  # noqa: E402,F401  (numpy-only reference)

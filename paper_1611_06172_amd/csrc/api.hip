@@ -369,4 +369,30 @@ int w2v_step_batch(int32_t B, int32_t N, int32_t K, const int32_t* targets,
   return ok();
 }
 
+size_t w2v_build_vocab_workspace_bytes(int32_t V_raw) {
+  if (V_raw <= 0) return 0;
+  return vocab_workspace_bytes(V_raw);
+}
+
+int w2v_build_vocab(const int32_t* raw, int64_t T, int32_t V_raw,
+                    int64_t min_count, int64_t* ranked_counts,
+                    int32_t* rank_of, int32_t* v_kept, int32_t* corpus_out,
+                    void* workspace, size_t workspace_bytes, void* stream) {
+  if (T < 0) return fail(W2V_EINVAL, "T must be >= 0");
+  if (T > 0 && raw == nullptr) return fail(W2V_EINVAL, "raw is NULL");
+  if (V_raw <= 0) return fail(W2V_EINVAL, "V_raw must be positive");
+  if (min_count < 0) return fail(W2V_EINVAL, "min_count must be >= 0");
+  if (ranked_counts == nullptr || rank_of == nullptr || v_kept == nullptr)
+    return fail(W2V_EINVAL, "ranked_counts, rank_of and v_kept must not be NULL");
+  if (workspace == nullptr || workspace_bytes < w2v_build_vocab_workspace_bytes(V_raw))
+    return failf(W2V_EINVAL, "workspace must hold %zu bytes",
+                 w2v_build_vocab_workspace_bytes(V_raw));
+  if (((uintptr_t)workspace & 255u) != 0)
+    return fail(W2V_EINVAL, "workspace must be 256-byte aligned");
+  hipError_t e = launch_vocab(raw, T, V_raw, min_count, ranked_counts, rank_of,
+                              v_kept, corpus_out, workspace, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "vocabulary launch");
+  return ok();
+}
+
 }  // extern "C"

@@ -73,6 +73,12 @@ int train_blocks_per_cu(int C, int nmax, int K);
 int grouped_blocks_per_cu(int C, int nmax, int K);
 hipError_t launch_grouped(int C, int nmax, const EpochArgs& a, int grid,
                           hipStream_t s);
+// Vocabulary of a raw id stream (vocab.hip).
+size_t vocab_workspace_bytes(int32_t V);
+hipError_t launch_vocab(const int32_t* raw, int64_t T, int32_t V,
+                        int64_t min_count, int64_t* ranked_counts,
+                        int32_t* rank_of, int32_t* v_kept, int32_t* corpus_out,
+                        void* workspace, hipStream_t s);
 // Algorithm 1 (per-pair) epoch kernel.
 int pairwise_blocks_per_cu(int C, int K);
 hipError_t launch_pairwise(int C, const EpochArgs& a, int grid, hipStream_t s);

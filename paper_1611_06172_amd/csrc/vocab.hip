@@ -1,0 +1,134 @@
+// Vocabulary of a raw id stream on the GPU: the step upstream of the
+// sampling tables (Sec. 2 trains on a corpus whose words are counted,
+// ranked by frequency and cut at a minimum count). It produces what the
+// rest of the library expects: ids ranked by frequency (id 0 the most
+// frequent word, which the atomic and split update tiers rely on), the
+// ranked counts for w2v_build_tables, and the corpus rewritten in ranked
+// ids with dropped words marked -1 (the epoch kernels skip such positions
+// before forming windows, as the original tool removes them from the
+// stream).
+//
+//   1. histogram of the raw ids (64-bit atomic counts; ids outside
+//      [0, V_raw) are not counted);
+//   2. a stable radix sort of the raw ids by count, descending, so equal
+//      counts keep increasing raw id order;
+//   3. rank r of sorted word s: new id r if its count reaches min_count,
+//      else -1; ranked counts out;
+//   4. the corpus rewritten through the rank map.
+#include <hip/hip_runtime.h>
+#include <hipcub/hipcub.hpp>
+
+#include "kernel_args.h"
+
+namespace w2v {
+
+__global__ __launch_bounds__(256) void k_vocab_count(const int32_t* raw,
+                                                     int64_t T, int32_t V,
+                                                     unsigned long long* counts) {
+  for (int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; p < T;
+       p += (int64_t)gridDim.x * blockDim.x) {
+    const int32_t x = raw[p];
+    if (x >= 0 && x < V) atomicAdd(&counts[x], 1ull);
+  }
+}
+
+__global__ __launch_bounds__(256) void k_vocab_zero(unsigned long long* c,
+                                                    int32_t V) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < V;
+       i += (int64_t)gridDim.x * blockDim.x)
+    c[i] = 0ull;
+}
+
+__global__ __launch_bounds__(256) void k_vocab_iota(int32_t* ids, int32_t V) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < V;
+       i += (int64_t)gridDim.x * blockDim.x)
+    ids[i] = (int32_t)i;
+}
+
+__global__ __launch_bounds__(256) void k_vocab_rank(
+    const unsigned long long* sorted_counts, const int32_t* sorted_ids,
+    int32_t V, int64_t min_count, int64_t* ranked_counts, int32_t* rank_of,
+    int32_t* v_kept) {
+  for (int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; r < V;
+       r += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t c = (int64_t)sorted_counts[r];
+    const bool keep = c >= min_count && c > 0;
+    rank_of[sorted_ids[r]] = keep ? (int32_t)r : -1;
+    ranked_counts[r] = keep ? c : 0;
+    // counts are non-increasing in r: the last kept rank fixes the size
+    const bool next_dropped =
+        r + 1 == V || !((int64_t)sorted_counts[r + 1] >= min_count &&
+                        sorted_counts[r + 1] > 0);
+    if (keep && next_dropped) *v_kept = (int32_t)(r + 1);
+    if (r == 0 && !keep) *v_kept = 0;
+  }
+}
+
+__global__ __launch_bounds__(256) void k_vocab_remap(const int32_t* raw,
+                                                     int64_t T, int32_t V,
+                                                     const int32_t* rank_of,
+                                                     int32_t* out) {
+  for (int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; p < T;
+       p += (int64_t)gridDim.x * blockDim.x) {
+    const int32_t x = raw[p];
+    out[p] = (x >= 0 && x < V) ? rank_of[x] : -1;
+  }
+}
+
+static size_t align256(size_t n) { return (n + 255) / 256 * 256; }
+
+static size_t sort_temp_bytes(int32_t V) {
+  size_t bytes = 0;
+  hipcub::DeviceRadixSort::SortPairsDescending(
+      (void*)nullptr, bytes, (const unsigned long long*)nullptr,
+      (unsigned long long*)nullptr, (const int32_t*)nullptr,
+      (int32_t*)nullptr, (int)V);
+  return bytes;
+}
+
+size_t vocab_workspace_bytes(int32_t V) {
+  // counts, sorted counts, ids, sorted ids, sort temporaries
+  return 2 * align256(sizeof(unsigned long long) * (size_t)V) +
+         2 * align256(sizeof(int32_t) * (size_t)V) + align256(sort_temp_bytes(V));
+}
+
+static int vocab_grid(int64_t n) {
+  const int64_t b = (n + 255) / 256;
+  return (int)(b < 8192 ? (b > 0 ? b : 1) : 8192);
+}
+
+hipError_t launch_vocab(const int32_t* raw, int64_t T, int32_t V,
+                        int64_t min_count, int64_t* ranked_counts,
+                        int32_t* rank_of, int32_t* v_kept, int32_t* corpus_out,
+                        void* workspace, hipStream_t s) {
+  char* w = (char*)workspace;
+  auto* counts = (unsigned long long*)w;
+  w += align256(sizeof(unsigned long long) * (size_t)V);
+  auto* sorted_counts = (unsigned long long*)w;
+  w += align256(sizeof(unsigned long long) * (size_t)V);
+  auto* ids = (int32_t*)w;
+  w += align256(sizeof(int32_t) * (size_t)V);
+  auto* sorted_ids = (int32_t*)w;
+  w += align256(sizeof(int32_t) * (size_t)V);
+  size_t temp_bytes = sort_temp_bytes(V);
+
+  hipLaunchKernelGGL(k_vocab_zero, dim3(vocab_grid(V)), dim3(256), 0, s, counts, V);
+  hipLaunchKernelGGL(k_vocab_count, dim3(vocab_grid(T)), dim3(256), 0, s, raw, T,
+                     V, counts);
+  hipLaunchKernelGGL(k_vocab_iota, dim3(vocab_grid(V)), dim3(256), 0, s, ids, V);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  e = hipcub::DeviceRadixSort::SortPairsDescending(
+      (void*)w, temp_bytes, (const unsigned long long*)counts, sorted_counts,
+      (const int32_t*)ids, sorted_ids, (int)V, 0, 64, s);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_vocab_rank, dim3(vocab_grid(V)), dim3(256), 0, s,
+                     sorted_counts, sorted_ids, V, min_count, ranked_counts,
+                     rank_of, v_kept);
+  if (corpus_out != nullptr)
+    hipLaunchKernelGGL(k_vocab_remap, dim3(vocab_grid(T)), dim3(256), 0, s, raw,
+                       T, V, rank_of, corpus_out);
+  return hipGetLastError();
+}
+
+}  // namespace w2v

@@ -58,6 +58,11 @@ def lib():
         _vp, _i64, _vp, _f32, _f32, _i32, _i32, _u64, _vp, _i32, _vp, _i32, _i32,
         _i32, _vp, ctypes.c_size_t, _i32, _i32, _vp]
     L.w2v_train_epoch.restype = ctypes.c_int
+    L.w2v_build_vocab_workspace_bytes.argtypes = [_i32]
+    L.w2v_build_vocab_workspace_bytes.restype = ctypes.c_size_t
+    L.w2v_build_vocab.argtypes = [_vp, _i64, _i32, _i64, _vp, _vp, _vp, _vp, _vp,
+                                  ctypes.c_size_t, _vp]
+    L.w2v_build_vocab.restype = ctypes.c_int
     L.w2v_train_epoch_workspace_bytes.argtypes = [_i32, _i32]
     L.w2v_train_epoch_workspace_bytes.restype = ctypes.c_size_t
     L.w2v_debug_minibatches.argtypes = [
@@ -316,3 +321,26 @@ def step_batch(targets, contexts, negatives, M_in, M_out, alpha=0.025, *,
         workspace.numel() * workspace.element_size(), _ptr(stats),
         _stream(stream)))
     return workspace
+
+
+def build_vocab(raw, V_raw: int, min_count: int = 0, remap: bool = True,
+                stream=None):
+    """Counts, frequency ranks and min-count cut of a raw id stream on the GPU
+    (w2v_build_vocab). Returns a dict of device tensors: ranked_counts
+    int64[V_raw], rank_of int32[V_raw], corpus int32[T] (or None) and V (an
+    int: this reads one value back from the device)."""
+    import torch
+    _dev(raw, torch.int32, "raw", 1)
+    dev = raw.device
+    T = raw.numel()
+    ranked = torch.empty(V_raw, dtype=torch.int64, device=dev)
+    rank_of = torch.empty(V_raw, dtype=torch.int32, device=dev)
+    v_kept = torch.empty(1, dtype=torch.int32, device=dev)
+    corpus = torch.empty(T, dtype=torch.int32, device=dev) if remap else None
+    ws = torch.empty(int(lib().w2v_build_vocab_workspace_bytes(V_raw)),
+                     dtype=torch.uint8, device=dev)
+    _check(lib().w2v_build_vocab(_ptr(raw), T, V_raw, int(min_count), _ptr(ranked),
+                                 _ptr(rank_of), _ptr(v_kept), _ptr(corpus), _ptr(ws),
+                                 ws.numel(), _stream(stream)))
+    return dict(ranked_counts=ranked, rank_of=rank_of, corpus=corpus,
+                V=int(v_kept.item()))

@@ -155,3 +155,21 @@ def test_hot_rows_rejects():
         args.update(kw)
         with pytest.raises(w2v.W2VError):
             w2v.hot_rows(c, **args)
+
+
+def vocab(**over):
+    args = dict(raw=FAKE, T=100, V=10, min_count=0, ranked=FAKE, rank_of=FAKE,
+                v_kept=FAKE, corpus=None, ws=0x100000, ws_bytes=1 << 20, stream=None)
+    args.update(over)
+    return w2v.lib().w2v_build_vocab(*args.values())
+
+
+@pytest.mark.parametrize("over,needle", [
+    (dict(T=-1), "T"), (dict(raw=None), "raw"), (dict(V=0), "V_raw"),
+    (dict(min_count=-1), "min_count"), (dict(ranked=None), "NULL"),
+    (dict(v_kept=None), "NULL"), (dict(ws=None), "workspace"),
+    (dict(ws_bytes=10), "workspace"), (dict(ws=0x100008), "aligned"),
+])
+def test_build_vocab_rejects(over, needle):
+    assert vocab(**over) == w2v.EINVAL
+    assert needle in w2v.lib().w2v_last_error().decode()
