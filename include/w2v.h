@@ -164,8 +164,8 @@ int64_t w2v_default_inflight(int32_t D, int32_t window, int32_t K);
  * target is masked for that member; all members' steps read the rows as
  * they were before the group and their updates to a row are summed; a
  * group's loss goes to the bucket of its first member. Needs 2 window G <=
- * 64 and G + K <= 64; the positions a group's windows span (2 window + G)
- * must fit a compiled input capacity (10, 16 or 32, see the shape limits).
+ * 64, 2 window + G <= 32 and G + K <= 32; G + K output columns are compiled
+ * up to 16 for D <= 384 and 10 for D <= 640, up to 32 for D <= 128.
  * Update path: a row with id < hot_rows receives fp32 atomic adds (no update
  * is lost under concurrency); a row with id >= hot_rows is written back as
  * (value read + update) by a store written through to device scope, so a

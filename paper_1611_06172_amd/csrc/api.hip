@@ -174,8 +174,11 @@ int w2v_train_epoch(const int32_t* corpus, int64_t T, int64_t pos_begin,
     return fail(W2V_EINVAL, "group must be 1, 2, 4 or 8");
   if (group > 1 && algorithm != W2V_ALGORITHM_HOGBATCH)
     return fail(W2V_EINVAL, "group > 1 needs the HogBatch algorithm");
-  if (group > 1 && (group * 2 * window > 64 || group + K > 64))
-    return fail(W2V_EINVAL, "group needs 2 * window * group <= 64 and group + K <= 64");
+  if (group > 1 && (group * 2 * window > 64 || 2 * window + group > 32 ||
+                    group + K > 32))
+    return fail(W2V_EINVAL,
+                "group needs 2 window group <= 64, 2 window + group <= 32 and "
+                "group + K <= 32");
   if (split_rows > 0) {
     if (workspace == nullptr) return fail(W2V_EINVAL, "workspace is NULL");
     if (workspace_bytes < w2v_train_epoch_workspace_bytes(split_rows, ld))
@@ -186,11 +189,15 @@ int w2v_train_epoch(const int32_t* corpus, int64_t T, int64_t pos_begin,
   const bool pairwise = algorithm == W2V_ALGORITHM_PAIRWISE;
   const bool grouped = group > 1;
   const int C = columns_for(D);
-  // distinct input rows of a group: at most the 2 window + group positions
-  // its members' windows span (2 window for one target)
-  const int nmax = inputs_cap_for(grouped ? 2 * window + group : 2 * window);
-  // Algorithm 1 handles one input word at a time: only D limits it.
-  if (C == 0 || nmax == 0 || (!pairwise && !train_shape_supported(C, nmax)))
+  const int nmax = inputs_cap_for(2 * window);
+  // a group's output columns: its targets and the shared negatives
+  const int omax = grouped ? group_outputs_cap_for(group + K) : 0;
+  // Algorithm 1 handles one input word at a time and a group its input rows
+  // in blocks: D (and a group's output columns) limit them.
+  const bool shape_ok = pairwise  ? C != 0
+                        : grouped ? C != 0 && grouped_shape_supported(C, omax)
+                                  : C != 0 && nmax != 0 && train_shape_supported(C, nmax);
+  if (!shape_ok)
     return failf(W2V_EUNSUPPORTED, "no compiled kernel for D=%d window=%d", D,
                  window);
   const int64_t n_sent = (pos_end - pos_begin + sentence_len - 1) / sentence_len;
@@ -229,7 +236,7 @@ int w2v_train_epoch(const int32_t* corpus, int64_t T, int64_t pos_begin,
   int64_t grid = max_inflight;
   if (grid == 0) {
     const int per_cu = pairwise  ? pairwise_blocks_per_cu(C, K)
-                       : grouped ? grouped_blocks_per_cu(C, nmax, K)
+                       : grouped ? grouped_blocks_per_cu(C, omax, K)
                                  : epoch_blocks_per_cu(C, nmax, window, K);
     const int cus = cu_count();
     grid = (int64_t)(per_cu > 0 ? per_cu : 1) * (cus > 0 ? cus : 1);
@@ -243,7 +250,7 @@ int w2v_train_epoch(const int32_t* corpus, int64_t T, int64_t pos_begin,
     if (e != hipSuccess) return hip_fail(e, "partial-row clear launch");
   }
   e = pairwise  ? launch_pairwise(C, a, (int)grid, s)
-      : grouped ? launch_grouped(C, nmax, a, (int)grid, s)
+      : grouped ? launch_grouped(C, omax, a, (int)grid, s)
                 : launch_train(C, nmax, a, (int)grid, s);
   if (e != hipSuccess) return hip_fail(e, "train kernel launch");
   if (split_rows > 0) {

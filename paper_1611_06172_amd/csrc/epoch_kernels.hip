@@ -121,9 +121,10 @@ __global__ __launch_bounds__(256) void k_part_fold(EpochArgs a) {
 // targets (group_core.h): per group, the members' input occurrences and the
 // output candidates (member targets, then the group's negatives) are staged
 // deduplicated with their group tables, then one snapshot step runs over the
-// group. Groups start at retained indices that are multiples of G (G divides
-// the 64-target batches).
-template <int C, int NMAX>
+// group (group_core.h) with up to OMAX output columns. Groups start at
+// retained indices that are multiples of G (G divides the 64-target
+// batches).
+template <int C, int OMAX>
 __global__ __launch_bounds__(kWave) void k_epoch_grouped(EpochArgs a) {
   __shared__ SentenceLds sl;
   __shared__ TargetBatch tb;
@@ -241,10 +242,7 @@ __global__ __launch_bounds__(kWave) void k_epoch_grouped(EpochArgs a) {
         n_mb += __popcll(members);
         sum_n += total;
         float loss_part = 0.f;
-        run_minibatch<C, NMAX, true, true, false, GroupError>(
-            a.M_in, a.M_out, a.M_in, a.M_out, a.ld, a.D, lane, n_in, n_out, 0.f,
-            a.hot_rows, mb, want_loss, loss_part, a.part, a.split_rows,
-            GroupError{&gl, G});
+        run_group<C, OMAX>(a, lane, n_in, n_out, mb, gl, G, want_loss, loss_part);
         if (want_loss) {
           const int qf = q0 + j0 + (int)__builtin_ctzll(members);
           const int64_t p = sb + sl.ret_off[qf];
@@ -344,16 +342,31 @@ hipError_t launch_train(int C, int nmax, const EpochArgs& a, int grid,
   return hipGetLastError();
 }
 
-static EpochKernel grouped_kernel_for(int C, int nmax) {
+#define W2V_GROUP_SHAPES(X) \
+  X(1, 10) X(2, 10) X(3, 10) X(4, 10) X(5, 10) X(6, 10) X(8, 10) X(10, 10) \
+  X(1, 16) X(2, 16) X(3, 16) X(4, 16) X(5, 16) X(6, 16) X(1, 32) X(2, 32)
+
+static EpochKernel grouped_kernel_for(int C, int omax) {
 #define W2V_PICK(c, n) \
-  if (C == c && nmax == n) return k_epoch_grouped<c, n>;
-  W2V_TRAIN_SHAPES(W2V_PICK)
+  if (C == c && omax == n) return k_epoch_grouped<c, n>;
+  W2V_GROUP_SHAPES(W2V_PICK)
 #undef W2V_PICK
   return nullptr;
 }
 
-int grouped_blocks_per_cu(int C, int nmax, int K) {
-  EpochKernel k = grouped_kernel_for(C, nmax);
+int group_outputs_cap_for(int n) {
+  if (n <= 10) return 10;
+  if (n <= 16) return 16;
+  if (n <= 32) return 32;
+  return 0;
+}
+
+bool grouped_shape_supported(int C, int omax) {
+  return grouped_kernel_for(C, omax) != nullptr;
+}
+
+int grouped_blocks_per_cu(int C, int omax, int K) {
+  EpochKernel k = grouped_kernel_for(C, omax);
   if (k == nullptr) return 0;
   int blocks = 0;
   const size_t dyn = sizeof(int32_t) * kWave * (size_t)(K > 0 ? K : 1);
@@ -363,9 +376,9 @@ int grouped_blocks_per_cu(int C, int nmax, int K) {
   return blocks;
 }
 
-hipError_t launch_grouped(int C, int nmax, const EpochArgs& a, int grid,
+hipError_t launch_grouped(int C, int omax, const EpochArgs& a, int grid,
                           hipStream_t s) {
-  EpochKernel k = grouped_kernel_for(C, nmax);
+  EpochKernel k = grouped_kernel_for(C, omax);
   if (k == nullptr) return hipErrorInvalidValue;
   hipLaunchKernelGGL(k, dim3(grid), dim3(kWave), epoch_dyn_lds(a), s, a);
   return hipGetLastError();

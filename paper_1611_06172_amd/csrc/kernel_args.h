@@ -69,9 +69,12 @@ bool train_shape_supported(int C, int nmax);
 int columns_for(int D);      // compiled C for a row length, 0 if none
 int inputs_cap_for(int n);   // compiled nmax for n input words, 0 if none
 int train_blocks_per_cu(int C, int nmax, int K);
-// HogBatch with negatives shared by groups of targets (any K: multi-block).
-int grouped_blocks_per_cu(int C, int nmax, int K);
-hipError_t launch_grouped(int C, int nmax, const EpochArgs& a, int grid,
+// HogBatch with negatives shared by groups of targets: omax = compiled
+// capacity of output columns (G + K).
+int group_outputs_cap_for(int n);
+bool grouped_shape_supported(int C, int omax);
+int grouped_blocks_per_cu(int C, int omax, int K);
+hipError_t launch_grouped(int C, int omax, const EpochArgs& a, int grid,
                           hipStream_t s);
 // Vocabulary of a raw id stream (vocab.hip).
 size_t vocab_workspace_bytes(int32_t V);

@@ -178,6 +178,49 @@ __device__ __forceinline__ float softplus(float z) {
   return fmaxf(z, 0.f) + log1pf(__expf(-fabsf(z)));
 }
 
+// Row access of a minibatch's live rows by tier: rows id < split_rows of
+// matrix m (0: input, 1: output) have partial rows part[((m split_rows + id)
+// kSplitParts + g) ld], g < kSplitParts, that every read adds and that take
+// the updates (atomically, in the partial row of this wavefront's group);
+// rows id < hot_rows take fp32 atomic adds; other rows a store of old + g.
+// kAccum64: fp64 atomic adds into a delta buffer instead (snapshot batches).
+template <int C, bool kAccum64>
+struct RowTiers {
+  float* part;
+  int split_rows;
+  int hot_rows;
+  int64_t ld;
+  int D;
+  int lane;
+
+  __device__ __forceinline__ float* part_base(int m, int id) const {
+    return part + (int64_t)(m * split_rows + id) * kSplitParts * ld;
+  }
+  // Adds the partial rows of a split row to its value as read.
+  __device__ __forceinline__ void add_split(int m, int id, float (&r)[C]) const {
+    if (id < split_rows) {
+      float* pb = part_base(m, id);
+#pragma unroll 1
+      for (int g = 0; g < kSplitParts; ++g) {
+        float t[C];
+        load_row<C, true>(pb, g, ld, D, lane, t);
+#pragma unroll
+        for (int c = 0; c < C; ++c) r[c] += t[c];
+      }
+    }
+  }
+  __device__ __forceinline__ void update(int m, void* W, int id,
+                                         const float (&old)[C],
+                                         const float (&g)[C]) const {
+    if (id < split_rows) {
+      update_row<C, false>(part_base(m, id), blockIdx.x % kSplitParts, ld, D,
+                           lane, kSplitParts, old, g);
+    } else {
+      update_row<C, kAccum64>(W, id, ld, D, lane, hot_rows, old, g);
+    }
+  }
+};
+
 // Error and loss of slot (input row li, output column lk) of a minibatch of
 // one target: column 0 is the target (label 1), the others negatives
 // (label 0); both scaled by the row and column multiplicities.
@@ -211,31 +254,10 @@ __device__ __forceinline__ void run_minibatch(
     int D, int lane, int n, int n_out, float alpha, int hot_rows,
     MinibatchLds& mb, bool want_loss, float& loss_part,
     float* part = nullptr, int split_rows = 0, const Err& err = Err()) {
-  auto part_base = [&](int m, int id) -> float* {
-    return part + (int64_t)(m * split_rows + id) * kSplitParts * ld;
-  };
-  // Adds the partial rows of a split row to its value as read.
-  auto read_split = [&](int m, int id, float (&r)[C]) {
-    if (id < split_rows) {
-      float* pb = part_base(m, id);
-#pragma unroll 1
-      for (int g = 0; g < kSplitParts; ++g) {
-        float t[C];
-        load_row<C, true>(pb, g, ld, D, lane, t);
-#pragma unroll
-        for (int c = 0; c < C; ++c) r[c] += t[c];
-      }
-    }
-  };
+  const RowTiers<C, kAccum64> io{part, split_rows, hot_rows, ld, D, lane};
+  auto read_split = [&](int m, int id, float (&r)[C]) { io.add_split(m, id, r); };
   auto update = [&](int m, void* W, int id, const float (&old)[C],
-                    const float (&g)[C]) {
-    if (id < split_rows) {
-      update_row<C, false>(part_base(m, id), blockIdx.x % kSplitParts, ld, D,
-                           lane, kSplitParts, old, g);
-    } else {
-      update_row<C, kAccum64>(W, id, ld, D, lane, hot_rows, old, g);
-    }
-  };
+                    const float (&g)[C]) { io.update(m, W, id, old, g); };
   constexpr int KB = kWave / NMAX;
   constexpr int kSlots = NMAX * KB;
   static_assert(KB >= 1 && kSlots <= kWave, "NMAX must be <= 64");

@@ -98,7 +98,7 @@ def train(**over):
     (dict(algorithm=1, split=1, ws=0x100000, ws_bytes=1 << 20), "pairwise"),
     (dict(group=3), "group"), (dict(group=0), "group"), (dict(group=16), "group"),
     (dict(group=2, algorithm=1), "group"), (dict(group=8, window=5), "group"),
-    (dict(group=8, window=2, K=60), "group"),
+    (dict(group=8, window=2, K=30), "group"), (dict(group=2, window=16, K=5), "group"),
 ])
 def test_train_epoch_rejects(over, needle):
     assert train(**over) == w2v.EINVAL
