@@ -24,10 +24,11 @@
 // evaluated lane-parallel and read back per slot with v_readlane, and the
 // two gradient products are lane-local FMAs.
 //
-// Update path (live matrices): rows with id < hot_rows receive fp32 atomic
-// adds (frequent words, whose concurrent updates would otherwise overwrite
-// each other), all other rows a plain store of (value read + update), the
-// Hogwild write the paper's threads perform (Sec. 1.1). Rows below
+// Update path (live matrices, RowTiers): rows with id < hot_rows receive
+// fp32 atomic adds (frequent words, whose concurrent updates would otherwise
+// overwrite each other), all other rows a store of (value read + update)
+// written through to device scope, the Hogwild write the paper's threads
+// perform (Sec. 1.1). Rows below
 // split_rows (the head of the Zipf law, written by nearly every concurrent
 // wavefront) are spread over kSplitParts partial rows: a wavefront adds its
 // update atomically to the partial row of its group (blockIdx mod
@@ -51,7 +52,7 @@ constexpr int kMaxInputs = 32;   // input words per minibatch (2 * max window)
 constexpr int kMaxOutputs = 65;  // target + up to 64 negatives
 constexpr int kSplitParts = W2V_SPLIT_PARTS;
 
-// Per-wavefront LDS staging of one minibatch's ids and its error block.
+// Per-wavefront LDS staging of one minibatch's ids and multiplicities.
 struct MinibatchLds {
   int raw_ctx[kMaxInputs];  // input words as formed
   int ctx[kMaxInputs];      // distinct input words (rows of M_in)
