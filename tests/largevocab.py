@@ -1,0 +1,46 @@
+"""The large-vocabulary workload on a prefix the oracle can follow (shared by
+the GPU test and the script that stores the oracle's numbers): 1e7 i.i.d.
+Zipf(1.07) tokens over V = 1e6 (numpy generator), D = 300, K = 5, window 5,
+t = 1e-4, tables from the workload's expected counts, one epoch. The
+held-out score is the mean SGNS loss per input word of 20,000 minibatches
+drawn independently of the corpus."""
+import numpy as np
+
+from paper_1611_06172_amd import inputs
+
+V, D, K, WINDOW, SAMPLE = 1_000_000, 300, 5, 5, 1e-4
+T = 10_000_000
+SEED = 1234
+
+
+def corpus():
+    return inputs.zipf_ids(T, V, 1.07, 8)
+
+
+def counts():
+    return np.rint(inputs.zipf_pmf(V, 1.07) * 1e9).astype(np.int64)
+
+
+def init_in():
+    return inputs.init_matrix(V, D, "uniform", 2)
+
+
+def heldout_ids(table):
+    t = inputs.zipf_ids(20_000, V, 1.07, 77)
+    c = inputs.zipf_ids((20_000, 6), V, 1.07, 78)
+    n = table[np.random.default_rng(79).integers(0, len(table), (20_000, K))]
+    return t, c, n
+
+
+def heldout_loss(M_in, M_out, t, c, n):
+    """Mean over minibatches and input words of -log sigma(a.o_t) -
+    sum_k log sigma(-a.o_k) (negatives equal to the target skipped), fp64."""
+    A = np.asarray(M_in, np.float64)[c]                      # [B, 6, D]
+    O = np.asarray(M_out, np.float64)[np.concatenate([t[:, None], n], 1)]  # [B, K+1, D]
+    X = np.einsum("bid,bkd->bik", A, O)
+    sign = np.ones(K + 1)
+    sign[1:] = -1
+    L = np.logaddexp(0.0, -X * sign)                         # softplus(-sign x)
+    mask = np.ones_like(L)
+    mask[:, :, 1:] = (n != t[:, None])[:, None, :]
+    return float((L * mask).sum() / (A.shape[0] * A.shape[1]))
