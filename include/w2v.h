@@ -66,6 +66,7 @@ extern "C" {
 /* The `algorithm` argument of w2v_train_epoch. */
 #define W2V_ALGORITHM_HOGBATCH 0  /* Sec. 1.1: minibatch, shared negatives */
 #define W2V_ALGORITHM_PAIRWISE 1  /* Alg. 1: per-pair SGD, private negatives */
+#define W2V_ALGORITHM_HOGBATCH_IMMEDIATE 2 /* Sec. 1.1, no pending input rows */
 
 /* Version of this ABI (major * 100 + minor). */
 int w2v_version(void);
@@ -117,6 +118,11 @@ int32_t w2v_hot_rows(const int64_t* counts, int32_t V, double neg_power,
  * W2V_E* code. */
 int64_t w2v_default_inflight(int32_t D, int32_t window, int32_t K);
 
+/* LDS slots per wavefront in which w2v_train_epoch (W2V_ALGORITHM_HOGBATCH,
+ * group 1) collects pending input-row updates for this shape on the current
+ * device (0: none), or a negative W2V_E* code. */
+int32_t w2v_pending_slots(int32_t D, int32_t window, int32_t K);
+
 /*
  * One Hogwild epoch (or a sentence-aligned part of one) of HogBatch SGD,
  * updating M_in and M_out in place on the GPU.
@@ -146,6 +152,22 @@ int64_t w2v_default_inflight(int32_t D, int32_t window, int32_t K);
  * to max_inflight sentences run concurrently and their updates interleave
  * without locks (Hogwild). max_inflight = 1 processes every minibatch in
  * sequence; 0 picks enough concurrent sentences to fill the GPU.
+ * Pending input rows (W2V_ALGORITHM_HOGBATCH with group 1): consecutive
+ * targets share most input words, so a wavefront adds the updates of a cold
+ * input row (id >= max(hot_rows, split_rows)) to one of
+ * w2v_pending_slots() LDS slots instead of M_in, reads the row as (M_in row
+ * + pending updates) while its word is in the window, and adds the slot to
+ * M_in atomically when it releases the word: when the slot is needed for
+ * another word, when 2 * window targets pass without the word, and at the
+ * end of the sentence. Every update reaches M_in before the call returns.
+ * With one sentence in flight this changes only the order of the fp32
+ * additions; with several, another sentence sees these updates late (as
+ * late as the word stays in this sentence's window) and never loses them.
+ * Rows below max(hot_rows, split_rows), which other sentences write
+ * constantly, take their updates at once: deferring those lets the
+ * concurrent sentences' stale steps pile up on them.
+ * W2V_ALGORITHM_HOGBATCH_IMMEDIATE applies every update at the end of its
+ * minibatch.
  * algorithm = W2V_ALGORITHM_PAIRWISE runs Alg. 1 instead (the original
  * per-pair Hogwild SGD, the paper's baseline) over the same targets, input
  * words and learning rates: each input word i in window order runs K+1
@@ -155,7 +177,7 @@ int64_t w2v_default_inflight(int32_t D, int32_t window, int32_t K);
  * that row moves right after its pair, and the M_in row of i moves once,
  * after its K+1 pairs. A target with any negative outside [0, V) is skipped
  * and counted in stats[3]. split_rows must be 0 with this algorithm.
- * group (HogBatch only; 1 is the paper's method): G in {2, 4, 8} shares the
+ * group (HogBatch, cached or not; 1 is the paper's method): G in {2, 4, 8} shares the
  * K negatives among G consecutive targets instead of one target's input
  * words (the sharing of Sec. 1.1 widened). The retained targets of a
  * sentence are cut at multiples of G; the members of a group (its targets

@@ -97,6 +97,15 @@ static int check_matrices(const float* M_in, const float* M_out, int32_t V,
   return W2V_OK;
 }
 
+// Ids below this never take a pending input-row slot: their updates go to
+// the matrix at the end of every minibatch. These are the rows other
+// sentences write constantly (atomic and split rows); with their updates
+// held back, concurrent sentences keep stepping from stale values and the
+// held-back steps add up, which makes a small vocabulary diverge.
+static int pending_from(int hot_rows, int split_rows) {
+  return hot_rows > split_rows ? hot_rows : split_rows;
+}
+
 static int epoch_blocks_per_cu(int C, int nmax, int window, int K) {
   (void)window;
   return train_blocks_per_cu(C, nmax, K);
@@ -144,6 +153,22 @@ int64_t w2v_default_inflight(int32_t D, int32_t window, int32_t K) {
   return (int64_t)per_cu * cus;
 }
 
+int32_t w2v_pending_slots(int32_t D, int32_t window, int32_t K) {
+  if (D < 1 || D > W2V_MAX_DIM)
+    return failf(W2V_EINVAL, "D must be in [1, %d]", W2V_MAX_DIM);
+  if (window < 1 || window > W2V_MAX_WINDOW)
+    return failf(W2V_EINVAL, "window must be in [1, %d]", W2V_MAX_WINDOW);
+  if (K < 0 || K > W2V_MAX_NEGATIVE)
+    return failf(W2V_EINVAL, "K must be in [0, %d]", W2V_MAX_NEGATIVE);
+  const int C = columns_for(D);
+  const int nmax = inputs_cap_for(2 * window);
+  if (C == 0 || nmax == 0 || !train_shape_supported(C, nmax))
+    return failf(W2V_EUNSUPPORTED, "no compiled kernel for D=%d window=%d", D,
+                 window);
+  ok();
+  return train_pending_slots(C, nmax, K);
+}
+
 int w2v_train_epoch(const int32_t* corpus, int64_t T, int64_t pos_begin,
                     int64_t pos_end, int32_t sentence_len, float* M_in,
                     float* M_out, int32_t V, int32_t D, int32_t ld,
@@ -164,15 +189,17 @@ int w2v_train_epoch(const int32_t* corpus, int64_t T, int64_t pos_begin,
     return fail(W2V_EINVAL, "n_buckets must be >= 1 with loss_buckets");
   if (max_inflight < 0) return fail(W2V_EINVAL, "max_inflight must be >= 0");
   if (hot_rows < 0) return fail(W2V_EINVAL, "hot_rows must be >= 0");
-  if (algorithm != W2V_ALGORITHM_HOGBATCH && algorithm != W2V_ALGORITHM_PAIRWISE)
-    return fail(W2V_EINVAL, "algorithm must be W2V_ALGORITHM_HOGBATCH or _PAIRWISE");
+  if (algorithm != W2V_ALGORITHM_HOGBATCH && algorithm != W2V_ALGORITHM_PAIRWISE &&
+      algorithm != W2V_ALGORITHM_HOGBATCH_IMMEDIATE)
+    return fail(W2V_EINVAL,
+                "algorithm must be W2V_ALGORITHM_HOGBATCH, _PAIRWISE or _HOGBATCH_IMMEDIATE");
   if (split_rows < 0 || split_rows > V)
     return fail(W2V_EINVAL, "split_rows must be in [0, V]");
   if (algorithm == W2V_ALGORITHM_PAIRWISE && split_rows != 0)
     return fail(W2V_EINVAL, "split_rows must be 0 with the pairwise algorithm");
   if (group != 1 && group != 2 && group != 4 && group != 8)
     return fail(W2V_EINVAL, "group must be 1, 2, 4 or 8");
-  if (group > 1 && algorithm != W2V_ALGORITHM_HOGBATCH)
+  if (group > 1 && algorithm == W2V_ALGORITHM_PAIRWISE)
     return fail(W2V_EINVAL, "group > 1 needs the HogBatch algorithm");
   if (group > 1 && (group * 2 * window > 64 || 2 * window + group > 32 ||
                     group + K > 32))
@@ -232,6 +259,10 @@ int w2v_train_epoch(const int32_t* corpus, int64_t T, int64_t pos_begin,
   a.split_rows = split_rows;
   a.part = (float*)workspace;
   a.group = group;
+  a.pend_slots = (pairwise || grouped || algorithm == W2V_ALGORITHM_HOGBATCH_IMMEDIATE)
+                     ? 0
+                     : train_pending_slots(C, nmax, K);
+  a.pend_from = pending_from(hot_rows, split_rows);
 
   int64_t grid = max_inflight;
   if (grid == 0) {

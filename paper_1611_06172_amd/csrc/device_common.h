@@ -179,6 +179,17 @@ __device__ __forceinline__ float wave_sum(float x) {
   return x;
 }
 
+// Minimum of one int over the wave (every lane gets it).
+__device__ __forceinline__ int wave_min(int x) {
+  x = min(x, __shfl_xor(x, 32));
+  x = min(x, __shfl_xor(x, 16));
+  x = min(x, __shfl_xor(x, 8));
+  x = min(x, __shfl_xor(x, 4));
+  x = min(x, __shfl_xor(x, 2));
+  x = min(x, __shfl_xor(x, 1));
+  return x;
+}
+
 // Value of x in lane l (l uniform; a compile-time constant after unrolling
 // makes this one v_readlane into a scalar register).
 __device__ __forceinline__ float lane_value(float x, int l) {

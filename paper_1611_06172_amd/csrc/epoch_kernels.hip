@@ -7,10 +7,14 @@
 //   3. runs those targets' minibatches in sentence order through the fused
 //      minibatch (sgns_core.h), so every minibatch of a sentence sees the
 //      updates of the ones before it, while minibatches of different
-//      sentences interleave without locks (Hogwild, Sec. 1.1).
+//      sentences interleave without locks (Hogwild, Sec. 1.1). The updates
+//      of input rows collect in a few LDS slots while their words stay in
+//      the window (assign_slots, PendingRows) and reach the matrix once.
 // It serves every compiled shape, including output blocks that take several
 // reductions. The export variant stops after step 2 and writes the
 // minibatches out.
+#include <climits>
+
 #include "group_core.h"
 #include "kernel_args.h"
 #include "sentence.h"
@@ -18,15 +22,88 @@
 
 namespace w2v {
 
+// Pending-update slots of a wavefront: lane s < nslots holds the word of
+// slot s (slot_id, -1 if free) and the retained index of the last target
+// that used it (slot_t). For the minibatch of target qj with distinct inputs
+// mb.ctx[0..n):
+//   * a word held in a slot is a hit;
+//   * any other word with id >= pend_from takes a free slot, else the least
+//     recently used slot no input of this minibatch holds (whose pending
+//     updates flush(s, id) first adds to the matrix), else none (its update
+//     goes to the matrix at once).
+// The choice goes to mb.slot (PendingRows). Slots unused for more than
+// `expire` targets are flushed and freed first, so no update stays pending
+// after its word has left the window for good; the caller flushes every
+// slot at the end of a sentence.
+template <int NMAX, class Flush>
+__device__ __forceinline__ void assign_slots(MinibatchLds& mb, int n, int qj,
+                                             int expire, int nslots,
+                                             int pend_from, int lane,
+                                             int& slot_id, int& slot_t,
+                                             const Flush& flush) {
+  const bool mine = lane < nslots;
+  for (uint64_t old = __ballot(mine && slot_id >= 0 && slot_t < qj - expire);
+       old != 0ull; old &= old - 1ull) {
+    const int s = __builtin_ctzll(old);
+    flush(s, __builtin_amdgcn_readlane(slot_id, s));
+    if (lane == s) slot_id = -1;
+  }
+  int code = -1;       // lane i < n: slot code of input i
+  uint32_t done = 0u;  // inputs settled by the first pass
+#pragma unroll
+  for (int i = 0; i < NMAX; ++i) {
+    if (i < n) {
+      const int id = uniform_int(mb.ctx[i]);
+      const uint64_t hm = __ballot(mine && slot_id == id);
+      if (hm != 0ull || id < pend_from) done |= 1u << i;
+      if (hm != 0ull) {
+        const int s = __builtin_ctzll(hm);
+        if (lane == i) code = kSlotHeld + s;
+        if (lane == s) slot_t = qj;
+      }
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < NMAX; ++i) {
+    if (i < n && ((done >> i) & 1u) == 0u) {
+      const int key = !mine ? INT_MAX : slot_id < 0 ? -1 : slot_t;
+      const int least = wave_min(key);
+      if (least < qj) {
+        const int s = __builtin_ctzll(__ballot(key == least));
+        if (least >= 0) flush(s, __builtin_amdgcn_readlane(slot_id, s));
+        if (lane == i) code = s;
+        if (lane == s) {
+          slot_id = uniform_int(mb.ctx[i]);
+          slot_t = qj;
+        }
+      }
+    }
+  }
+  if (lane < n) mb.slot[lane] = code;
+  __syncthreads();
+}
+
 template <int C, int NMAX, bool kMulti, bool kExport>
 __global__ __launch_bounds__(kWave) void k_epoch(EpochArgs a) {
   __shared__ SentenceLds sl;
   __shared__ TargetBatch tb;
   __shared__ MinibatchLds mb;
-  extern __shared__ int32_t negs_lds[];  // [kWave][K]
+  extern __shared__ int32_t negs_lds[];  // [kWave][K], then the row slots
   const int lane = threadIdx.x;
   const int K = a.K;
   const bool want_loss = a.loss != nullptr;
+  float* const slot_rows = reinterpret_cast<float*>(negs_lds + kWave * (K > 0 ? K : 1));
+  const int nslots = kExport ? 0 : a.pend_slots;
+  int slot_id = -1, slot_t = 0;
+  const RowTiers<C, false> io{a.part, a.split_rows, a.hot_rows, a.ld, a.D, lane};
+  // Adds the pending updates of slot s to the M_in row of word id.
+  auto flush = [&](int s, int id) {
+    const float* p = slot_rows + s * (kWave * C) + lane;
+    float d[C];
+#pragma unroll
+    for (int c = 0; c < C; ++c) d[c] = p[kWave * c];
+    io.add(0, a.M_in, id, d);
+  };
 
   int64_t n_mb = 0, sum_n = 0, raw = 0, rejected = 0;
   double lsum = 0.0, lcnt = 0.0;
@@ -63,11 +140,17 @@ __global__ __launch_bounds__(kWave) void k_epoch(EpochArgs a) {
           const int n_in = stage_inputs(lane, ctx_id, lane < n, mb);
           const int neg = lane < K ? negs_lds[j * K + lane] : 0;
           const int n_out = stage_outputs(lane, sl.ret_id[qj], neg, K, mb);
+          if (nslots > 0)
+            assign_slots<NMAX>(mb, n_in, qj, 2 * a.w, nslots, a.pend_from, lane,
+                               slot_id, slot_t, flush);
+          else if (lane < n_in)
+            mb.slot[lane] = -1;
+          const PendingRows pend{slot_rows, mb.slot};
           float loss_part = 0.f;
           run_minibatch<C, NMAX, kMulti, true, false>(
               a.M_in, a.M_out, a.M_in, a.M_out, a.ld, a.D, lane, n_in, n_out,
               uniform_float(tb.alpha[j]), a.hot_rows, mb, want_loss,
-              loss_part, a.part, a.split_rows);
+              loss_part, a.part, a.split_rows, TargetError(), pend);
           if (want_loss) {
             const int64_t p = sb + sl.ret_off[qj];
             const int b = (int)(p * (int64_t)a.n_buckets / a.T);
@@ -81,6 +164,14 @@ __global__ __launch_bounds__(kWave) void k_epoch(EpochArgs a) {
         }
       }
       __syncthreads();
+    }
+    if constexpr (!kExport) {
+      for (uint64_t held = __ballot(lane < nslots && slot_id >= 0); held != 0ull;
+           held &= held - 1ull) {
+        const int s = __builtin_ctzll(held);
+        flush(s, __builtin_amdgcn_readlane(slot_id, s));
+      }
+      slot_id = -1;
     }
   }
   if (want_loss && bucket >= 0) flush_loss(a.loss, bucket, lsum, lcnt, lane);
@@ -319,8 +410,34 @@ int inputs_cap_for(int n) {
   return 0;
 }
 
+static size_t negatives_lds(int K) {
+  return sizeof(int32_t) * (size_t)kWave * (size_t)(K > 0 ? K : 1);
+}
+
 static size_t epoch_dyn_lds(const EpochArgs& a) {
-  return sizeof(int32_t) * (size_t)kWave * (size_t)(a.K > 0 ? a.K : 1);
+  return negatives_lds(a.K);
+}
+
+static size_t slot_bytes(int C) { return sizeof(float) * (size_t)kWave * C; }
+
+constexpr int kMaxPendingSlots = 16;
+
+int train_pending_slots(int C, int nmax, int K) {
+  EpochKernel k = train_kernel_for(C, nmax, K);
+  if (k == nullptr) return 0;
+  int base = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&base, k, kWave,
+                                                   negatives_lds(K)) != hipSuccess ||
+      base <= 0)
+    return 0;
+  for (int n = kMaxPendingSlots; n >= 2; --n) {
+    int blocks = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(
+            &blocks, k, kWave, negatives_lds(K) + n * slot_bytes(C)) != hipSuccess)
+      return 0;
+    if (blocks >= base) return n;
+  }
+  return 0;
 }
 
 int train_blocks_per_cu(int C, int nmax, int K) {
@@ -338,7 +455,8 @@ hipError_t launch_train(int C, int nmax, const EpochArgs& a, int grid,
                         hipStream_t s) {
   EpochKernel k = train_kernel_for(C, nmax, a.K);
   if (k == nullptr) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(k, dim3(grid), dim3(kWave), epoch_dyn_lds(a), s, a);
+  hipLaunchKernelGGL(k, dim3(grid), dim3(kWave),
+                     epoch_dyn_lds(a) + a.pend_slots * slot_bytes(C), s, a);
   return hipGetLastError();
 }
 

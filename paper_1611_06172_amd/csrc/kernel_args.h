@@ -30,6 +30,8 @@ struct EpochArgs {
   int32_t split_rows;      // ids below this use partial rows in `part`
   int32_t group;           // consecutive targets sharing one negative draw
   float* part;             // [2][split_rows][kSplitParts][ld] partial rows
+  int32_t pend_slots;      // LDS pending input-row slots per wavefront (0: none)
+  int32_t pend_from;       // ids below this never take a pending slot
   // export outputs (minibatch export only)
   int32_t* out_targets;
   int32_t* out_ctx;
@@ -69,6 +71,9 @@ bool train_shape_supported(int C, int nmax);
 int columns_for(int D);      // compiled C for a row length, 0 if none
 int inputs_cap_for(int n);   // compiled nmax for n input words, 0 if none
 int train_blocks_per_cu(int C, int nmax, int K);
+// Pending input-row slots that fit beside the training kernel's LDS without
+// lowering its occupancy (0 if fewer than two fit).
+int train_pending_slots(int C, int nmax, int K);
 // HogBatch with negatives shared by groups of targets: omax = compiled
 // capacity of output columns (G + K).
 int group_outputs_cap_for(int n);

@@ -37,6 +37,14 @@
 // one XCD only and nothing is hidden from a reader. Snapshot batches add
 // their updates with fp64 atomics into a delta buffer instead.
 //
+// Pending input-row updates (PendingRows): consecutive targets of a
+// sentence share most of their input words, so a training wavefront adds
+// the updates of an input row to an LDS slot instead of the matrix, reads
+// the row as (matrix row + its pending updates) while the word stays in the
+// window, and adds the slot to the matrix once, atomically, when it lets
+// the word go. The row traffic of the minibatch path is dominated by its
+// writes; this turns about 2 window writes of an input row into one.
+//
 // Output columns are processed in blocks of KB = 64 / NMAX so that one
 // block's partials fill one reduction; with K+1 <= KB (the paper's K = 5 with
 // up to ten input words) the whole minibatch is a single block, compiled
@@ -60,6 +68,7 @@ struct MinibatchLds {
   int raw[kWave];           // negatives as drawn
   int out[kMaxOutputs];     // [0] target, then distinct unmasked negatives
   float wgt[kMaxOutputs];   // multiplicity of each output column
+  int slot[kMaxInputs];     // pending-update slot of each input row (PendingRows)
 };
 
 // Stages the input rows: the lanes with `present` set hold the input words
@@ -210,6 +219,15 @@ struct RowTiers {
       }
     }
   }
+  // Adds g to row id atomically whatever its tier (pending updates).
+  __device__ __forceinline__ void add(int m, float* W, int id,
+                                      const float (&g)[C]) const {
+    if (id < split_rows)
+      update_row<C, false>(part_base(m, id), blockIdx.x % kSplitParts, ld, D,
+                           lane, kSplitParts, g, g);
+    else
+      update_row<C, false>(W, id, ld, D, lane, id + 1, g, g);
+  }
   __device__ __forceinline__ void update(int m, void* W, int id,
                                          const float (&old)[C],
                                          const float (&g)[C]) const {
@@ -240,21 +258,73 @@ struct TargetError {
   }
 };
 
+// Input-row updates applied to the matrix at once (no pending slots).
+struct NoPendingRows {
+  template <int C>
+  __device__ __forceinline__ void add_pending(int, int, float (&)[C]) const {}
+  template <int C>
+  __device__ __forceinline__ bool defer(int, int, const float (&)[C]) const {
+    return false;
+  }
+};
+
+// rows: [slots][64 C] floats in LDS, the updates a wavefront has made to an
+// input row and not yet added to the matrix (lane l's columns l + 64c at
+// offset 64c + l). slot[i] for distinct input i of the minibatch: -1: no
+// slot, its update goes to the matrix at once; s < kSlotHeld: slot s,
+// empty, which takes this minibatch's update; kSlotHeld + s: slot s holds
+// pending updates of this word, which every read adds and to which this
+// minibatch's update is added.
+constexpr int kSlotHeld = 64;
+
+struct PendingRows {
+  float* rows;
+  const int* slot;
+
+  template <int C>
+  __device__ __forceinline__ void add_pending(int i, int lane,
+                                              float (&r)[C]) const {
+    const int s = uniform_int(slot[i]);
+    if (s < kSlotHeld) return;
+    const float* p = rows + (s - kSlotHeld) * (kWave * C) + lane;
+#pragma unroll
+    for (int c = 0; c < C; ++c) r[c] += p[kWave * c];
+  }
+  template <int C>
+  __device__ __forceinline__ bool defer(int i, int lane,
+                                        const float (&g)[C]) const {
+    const int s = uniform_int(slot[i]);
+    if (s < 0) return false;
+    float* p = rows + (s & (kSlotHeld - 1)) * (kWave * C) + lane;
+    if (s >= kSlotHeld) {
+#pragma unroll
+      for (int c = 0; c < C; ++c) p[kWave * c] += g[c];
+    } else {
+#pragma unroll
+      for (int c = 0; c < C; ++c) p[kWave * c] = g[c];
+    }
+    return true;
+  }
+};
+
 // Runs one minibatch. Rin/Rout: where rows are read; Win/Wout: where updates
 // go (the same fp32 matrices, or fp64 delta buffers with the same row stride
 // when kAccum64). n distinct input rows (n <= NMAX) in mb.ctx/mb.cwgt, n_out
 // distinct output columns in mb.out/mb.wgt. Rows id < split_rows of matrix m
 // (0: input, 1: output) have partial rows part[((m split_rows + id)
 // kSplitParts + g) ld], g < kSplitParts (live matrices only). `err` gives
-// the error of a slot (TargetError for one target). Every lane returns its
-// share of the minibatch loss in `loss_part` when want_loss is set.
+// the error of a slot (TargetError for one target); `pend` holds input-row
+// updates not yet added to the matrix (NoPendingRows: none).
+// Every lane returns its share of the minibatch loss in `loss_part` when
+// want_loss is set.
 template <int C, int NMAX, bool kMulti, bool kLiveRead, bool kAccum64,
-          class Err = TargetError>
+          class Err = TargetError, class Pend = NoPendingRows>
 __device__ __forceinline__ void run_minibatch(
     const float* Rin, const float* Rout, void* Win, void* Wout, int64_t ld,
     int D, int lane, int n, int n_out, float alpha, int hot_rows,
     MinibatchLds& mb, bool want_loss, float& loss_part,
-    float* part = nullptr, int split_rows = 0, const Err& err = Err()) {
+    float* part = nullptr, int split_rows = 0, const Err& err = Err(),
+    const Pend& pend = Pend()) {
   const RowTiers<C, kAccum64> io{part, split_rows, hot_rows, ld, D, lane};
   auto read_split = [&](int m, int id, float (&r)[C]) { io.add_split(m, id, r); };
   auto update = [&](int m, void* W, int id, const float (&old)[C],
@@ -270,6 +340,7 @@ __device__ __forceinline__ void run_minibatch(
     if (i < n) {
       load_row<C, kLiveRead>(Rin, uniform_int(mb.ctx[i]), ld, D, lane, a[i]);
       read_split(0, uniform_int(mb.ctx[i]), a[i]);
+      pend.template add_pending<C>(i, lane, a[i]);
     } else {
 #pragma unroll
       for (int c = 0; c < C; ++c) a[i][c] = 0.f;
@@ -358,7 +429,8 @@ __device__ __forceinline__ void run_minibatch(
 #pragma unroll
           for (int c = 0; c < C; ++c) ga[i][c] = g[c];
         } else {
-          update(0, Win, uniform_int(mb.ctx[i]), a[i], g);
+          if (!pend.template defer<C>(i, lane, g))
+            update(0, Win, uniform_int(mb.ctx[i]), a[i], g);
         }
       }
     }
@@ -367,8 +439,10 @@ __device__ __forceinline__ void run_minibatch(
   if constexpr (kMulti) {
 #pragma unroll
     for (int i = 0; i < NMAX; ++i)
-      if (i < n)
-        update(0, Win, uniform_int(mb.ctx[i]), a[i], ga[i]);
+      if (i < n) {
+        if (!pend.template defer<C>(i, lane, ga[i]))
+          update(0, Win, uniform_int(mb.ctx[i]), a[i], ga[i]);
+      }
   }
 }
 

@@ -77,12 +77,15 @@ __global__ __launch_bounds__(256) void k_vocab_remap(const int32_t* raw,
 
 static size_t align256(size_t n) { return (n + 255) / 256 * 256; }
 
+// Temporary bytes of the sort; 0 if the size query fails, in which case the
+// sort itself reports the error (its temporaries are then too small).
 static size_t sort_temp_bytes(int32_t V) {
   size_t bytes = 0;
-  hipcub::DeviceRadixSort::SortPairsDescending(
-      (void*)nullptr, bytes, (const unsigned long long*)nullptr,
-      (unsigned long long*)nullptr, (const int32_t*)nullptr,
-      (int32_t*)nullptr, (int)V);
+  if (hipcub::DeviceRadixSort::SortPairsDescending(
+          (void*)nullptr, bytes, (const unsigned long long*)nullptr,
+          (unsigned long long*)nullptr, (const int32_t*)nullptr,
+          (int32_t*)nullptr, (int)V) != hipSuccess)
+    return 0;
   return bytes;
 }
 

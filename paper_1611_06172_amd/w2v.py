@@ -73,6 +73,8 @@ def lib():
     L.w2v_hot_rows.restype = ctypes.c_int32
     L.w2v_default_inflight.argtypes = [_i32, _i32, _i32]
     L.w2v_default_inflight.restype = ctypes.c_int64
+    L.w2v_pending_slots.argtypes = [_i32, _i32, _i32]
+    L.w2v_pending_slots.restype = ctypes.c_int32
     L.w2v_step_batch_workspace_bytes.argtypes = [_i32, _i32]
     L.w2v_step_batch_workspace_bytes.restype = ctypes.c_size_t
     L.w2v_step_batch.argtypes = [
@@ -165,7 +167,16 @@ def default_inflight(D: int, window: int = 5, K: int = 5) -> int:
     return n
 
 
-ALGORITHMS = {"hogbatch": 0, "pairwise": 1}
+def pending_slots(D: int, window: int = 5, K: int = 5) -> int:
+    """LDS slots per wavefront in which HogBatch training collects pending
+    updates of cold input rows (0: none)."""
+    n = int(lib().w2v_pending_slots(D, window, K))
+    if n < 0:
+        _check(n)
+    return n
+
+
+ALGORITHMS = {"hogbatch": 0, "pairwise": 1, "hogbatch_immediate": 2}
 
 
 def train_epoch(corpus, M_in, M_out, neg_table, keep_thresh=None, *,
@@ -184,7 +195,10 @@ def train_epoch(corpus, M_in, M_out, neg_table, keep_thresh=None, *,
     split_rows: ids below it are updated through per-XCD partial rows that
     every read sums (see w2v_train_epoch); workspace (a device byte tensor of
     train_epoch_workspace_bytes(split_rows, ld)) is allocated when None.
-    algorithm: "hogbatch" (Sec. 1.1) or "pairwise" (Alg. 1, the baseline).
+    algorithm: "hogbatch" (Sec. 1.1; cold input rows collect their updates
+        in LDS while their word is in the window, see w2v_train_epoch),
+        "hogbatch_immediate" (every update applied at the end of its
+        minibatch) or "pairwise" (Alg. 1, the baseline).
     group: consecutive targets sharing one draw of negatives (1: HogBatch as
     in the paper; 2, 4, 8: the sharing widened across targets)."""
     import torch

@@ -94,7 +94,7 @@ def train(**over):
     (dict(split=11), "split_rows"), (dict(split=2), "workspace"),
     (dict(split=2, ws=0x100000, ws_bytes=2 * 2 * 8 * 8 * 4 - 1), "workspace"),
     (dict(split=2, ws=0x100010, ws_bytes=1 << 20), "aligned"),
-    (dict(algorithm=2), "algorithm"), (dict(algorithm=-1), "algorithm"),
+    (dict(algorithm=3), "algorithm"), (dict(algorithm=-1), "algorithm"),
     (dict(algorithm=1, split=1, ws=0x100000, ws_bytes=1 << 20), "pairwise"),
     (dict(group=3), "group"), (dict(group=0), "group"), (dict(group=16), "group"),
     (dict(group=2, algorithm=1), "group"), (dict(group=8, window=5), "group"),
@@ -172,4 +172,13 @@ def vocab(**over):
 ])
 def test_build_vocab_rejects(over, needle):
     assert vocab(**over) == w2v.EINVAL
+    assert needle in w2v.lib().w2v_last_error().decode()
+
+
+@pytest.mark.parametrize("args,needle", [
+    ((0, 5, 5), "D"), ((641, 5, 5), "D"), ((300, 0, 5), "window"),
+    ((300, 17, 5), "window"), ((300, 5, -1), "K"), ((300, 5, 65), "K"),
+])
+def test_pending_slots_rejects(args, needle):
+    assert w2v.lib().w2v_pending_slots(*args) == w2v.EINVAL
     assert needle in w2v.lib().w2v_last_error().decode()
