@@ -177,7 +177,7 @@ int32_t w2v_pending_slots(int32_t D, int32_t window, int32_t K);
  * that row moves right after its pair, and the M_in row of i moves once,
  * after its K+1 pairs. A target with any negative outside [0, V) is skipped
  * and counted in stats[3]. split_rows must be 0 with this algorithm.
- * group (HogBatch, cached or not; 1 is the paper's method): G in {2, 4, 8} shares the
+ * group (HogBatch algorithms; 1 is the paper's method): G in {2, 4, 8} shares the
  * K negatives among G consecutive targets instead of one target's input
  * words (the sharing of Sec. 1.1 widened). The retained targets of a
  * sentence are cut at multiples of G; the members of a group (its targets
