@@ -84,6 +84,10 @@ def main():
                          "spread over per-XCD partial rows (w2v_hot_rows)")
     ap.add_argument("--split-rows", type=int, default=-1,
                     help="override the split-row threshold (-1: model)")
+    ap.add_argument("--split-max", type=int, default=2,
+                    help="cap on the model's split rows: every read of a split "
+                         "row sums its 8 partial rows, which outweighs the "
+                         "spread atomics beyond the first one or two words")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="run a 1 GiB device copy first (counter calibration)")
     ap.add_argument("--cpu-sample-tokens", type=int, default=2_000_000)
@@ -124,8 +128,9 @@ def main():
            w2v.hot_rows(counts, sample_t=args.sample, window=W, K=K,
                         inflight=inflight, tol=args.hot_tol))
     split = (args.split_rows if args.split_rows >= 0 else
-             w2v.hot_rows(counts, sample_t=args.sample, window=W, K=K,
-                          inflight=inflight, tol=args.split_tol))
+             min(args.split_max,
+                 w2v.hot_rows(counts, sample_t=args.sample, window=W, K=K,
+                              inflight=inflight, tol=args.split_tol)))
     if args.algorithm == "pairwise":
         split = 0  # partial rows serve the HogBatch kernel only
     pend_slots = (w2v.pending_slots(D, W, K)

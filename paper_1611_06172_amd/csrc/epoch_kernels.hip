@@ -410,6 +410,28 @@ int inputs_cap_for(int n) {
   return 0;
 }
 
+// gfx950 gives each CU 160 KB of LDS and allocates it to a workgroup in
+// granules of 1280 bytes. The runtime's occupancy query admits requests that
+// the granules do not: at D = 100, K = 5 it allowed 12 workgroups per CU
+// with 12,808 bytes each, 12 x 10 granules would need 168,960 bytes, and a
+// twelfth of the persistent grid then waited for a free CU (-34%
+// throughput). Both limits apply.
+constexpr size_t kLdsPerCu = 160 * 1024;
+constexpr size_t kLdsGranule = 1280;
+
+int resident_blocks_per_cu(const void* kernel, size_t dyn_lds) {
+  int blocks = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, kernel, kWave,
+                                                   dyn_lds) != hipSuccess)
+    return 0;
+  hipFuncAttributes attr{};
+  if (hipFuncGetAttributes(&attr, kernel) != hipSuccess) return 0;
+  const size_t per = (attr.sharedSizeBytes + dyn_lds + kLdsGranule - 1) /
+                     kLdsGranule * kLdsGranule;
+  const int by_lds = (int)(kLdsPerCu / per);
+  return blocks < by_lds ? blocks : by_lds;
+}
+
 static size_t negatives_lds(int K) {
   return sizeof(int32_t) * (size_t)kWave * (size_t)(K > 0 ? K : 1);
 }
@@ -425,30 +447,19 @@ constexpr int kMaxPendingSlots = 16;
 int train_pending_slots(int C, int nmax, int K) {
   EpochKernel k = train_kernel_for(C, nmax, K);
   if (k == nullptr) return 0;
-  int base = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&base, k, kWave,
-                                                   negatives_lds(K)) != hipSuccess ||
-      base <= 0)
-    return 0;
-  for (int n = kMaxPendingSlots; n >= 2; --n) {
-    int blocks = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(
-            &blocks, k, kWave, negatives_lds(K) + n * slot_bytes(C)) != hipSuccess)
-      return 0;
-    if (blocks >= base) return n;
-  }
+  const void* f = reinterpret_cast<const void*>(k);
+  const int base = resident_blocks_per_cu(f, negatives_lds(K));
+  if (base <= 0) return 0;
+  for (int n = kMaxPendingSlots; n >= 2; --n)
+    if (resident_blocks_per_cu(f, negatives_lds(K) + n * slot_bytes(C)) >= base)
+      return n;
   return 0;
 }
 
 int train_blocks_per_cu(int C, int nmax, int K) {
   EpochKernel k = train_kernel_for(C, nmax, K);
   if (k == nullptr) return 0;
-  int blocks = 0;
-  const size_t dyn = sizeof(int32_t) * kWave * (size_t)(K > 0 ? K : 1);
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, k, kWave, dyn) !=
-      hipSuccess)
-    return 0;
-  return blocks;
+  return resident_blocks_per_cu(reinterpret_cast<const void*>(k), negatives_lds(K));
 }
 
 hipError_t launch_train(int C, int nmax, const EpochArgs& a, int grid,
@@ -486,12 +497,7 @@ bool grouped_shape_supported(int C, int omax) {
 int grouped_blocks_per_cu(int C, int omax, int K) {
   EpochKernel k = grouped_kernel_for(C, omax);
   if (k == nullptr) return 0;
-  int blocks = 0;
-  const size_t dyn = sizeof(int32_t) * kWave * (size_t)(K > 0 ? K : 1);
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, k, kWave, dyn) !=
-      hipSuccess)
-    return 0;
-  return blocks;
+  return resident_blocks_per_cu(reinterpret_cast<const void*>(k), negatives_lds(K));
 }
 
 hipError_t launch_grouped(int C, int omax, const EpochArgs& a, int grid,

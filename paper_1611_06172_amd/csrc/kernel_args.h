@@ -57,6 +57,10 @@ struct StepArgs {
   int64_t* stats;
 };
 
+// Workgroups of one wavefront of `kernel` resident per CU with `dyn_lds`
+// bytes of dynamic LDS (0 on a failed query).
+int resident_blocks_per_cu(const void* kernel, size_t dyn_lds);
+
 // Launchers (defined next to the kernels). Return a hipError_t.
 // C: columns per lane (D <= 64 C); nmax: max input words per minibatch.
 hipError_t launch_train(int C, int nmax, const EpochArgs& a, int grid,

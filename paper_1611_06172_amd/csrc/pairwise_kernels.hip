@@ -240,12 +240,8 @@ static PairKernel pairwise_kernel_for(int C) {
 int pairwise_blocks_per_cu(int C, int K) {
   PairKernel k = pairwise_kernel_for(C);
   if (k == nullptr) return 0;
-  int blocks = 0;
   const size_t dyn = sizeof(int32_t) * kWave * (size_t)(K > 0 ? K : 1);
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, k, kWave, dyn) !=
-      hipSuccess)
-    return 0;
-  return blocks;
+  return resident_blocks_per_cu(reinterpret_cast<const void*>(k), dyn);
 }
 
 hipError_t launch_pairwise(int C, const EpochArgs& a, int grid, hipStream_t s) {

@@ -356,8 +356,8 @@ __device__ __forceinline__ void run_minibatch(
       for (int c = 0; c < C; ++c) ga[i][c] = 0.f;
   }
 
-  for (int k0 = 0; k0 < (kMulti ? n_out : 1); k0 += KB) {
-    float o[KB][C];
+  // Output rows of the block starting at column k0 (zero past n_out).
+  auto load_block = [&](int k0, float (&o)[KB][C]) {
 #pragma unroll
     for (int kk = 0; kk < KB; ++kk) {
       if (k0 + kk < n_out) {
@@ -368,6 +368,29 @@ __device__ __forceinline__ void run_minibatch(
 #pragma unroll
         for (int c = 0; c < C; ++c) o[kk][c] = 0.f;
       }
+    }
+  };
+  // With several blocks, the next block's rows are loaded while this one is
+  // computed and written; they are other rows than this block's (columns
+  // are distinct), so every row is still read before the minibatch writes
+  // it. The KB x C extra registers cost the C = 5, KB = 6 kernel its second
+  // wavefront per SIMD (1e8 tokens, D = 300, K = 15: 123 -> 91 Mwords/s),
+  // so it keeps the serial loads; the others gain (D = 100, K = 15: 144 ->
+  // 180; D = 600, K = 15: 54 -> 63).
+  constexpr bool kPrefetch = kMulti && (C * KB <= 24 || C >= 6);
+  float next[kPrefetch ? KB : 1][C];
+  if constexpr (kPrefetch) load_block(0, next);
+
+  for (int k0 = 0; k0 < (kMulti ? n_out : 1); k0 += KB) {
+    float o[KB][C];
+    if constexpr (kPrefetch) {
+#pragma unroll
+      for (int kk = 0; kk < KB; ++kk)
+#pragma unroll
+        for (int c = 0; c < C; ++c) o[kk][c] = next[kk][c];
+      if (k0 + KB < n_out) load_block(k0 + KB, next);
+    } else {
+      load_block(k0, o);
     }
 
     // Per-lane partial logits, slot s = i*KB + kk, formed as the reduction
