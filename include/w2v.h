@@ -313,6 +313,34 @@ int w2v_step_batch(int32_t B, int32_t N, int32_t K, const int32_t* targets,
                    void* workspace, size_t workspace_bytes, int64_t* stats,
                    void* stream);
 
+/* Bytes of workspace w2v_step_batch_sorted needs for B minibatches of N
+ * input slots and K negatives over V rows of stride ld (0 on invalid
+ * arguments or a failed query): staging rows for every update, sort keys
+ * and values, per-chunk partial sums and the sort's temporaries. */
+size_t w2v_step_batch_sorted_workspace_bytes(int32_t B, int32_t N, int32_t K,
+                                             int32_t V, int32_t ld);
+
+/*
+ * The step of w2v_step_batch (same arguments, readings and limits) with
+ * every row's updates summed in one fixed order: each minibatch's updates
+ * are written to staging rows, sorted by row id with a stable radix sort
+ * (so a row's updates stay in minibatch order) and summed per row in fp64
+ * in that order, in chunks of 64 whose partial sums are added in chunk
+ * order. The result is the same bits on every run, and no atomics are
+ * used. It may differ from w2v_step_batch, whose fp64 atomics add in
+ * arrival order, in the last fp32 bit of an element.
+ * Additional limit: B (N + K + 1) must fit in int32. workspace: device,
+ * >= w2v_step_batch_sorted_workspace_bytes(B, N, K, V, ld) bytes, 256-byte
+ * aligned, caller-owned, contents need not be initialised; calls that
+ * overlap in time must not share it.
+ */
+int w2v_step_batch_sorted(int32_t B, int32_t N, int32_t K, const int32_t* targets,
+                          const int32_t* contexts, const int32_t* negatives,
+                          const float* alpha, float alpha_scalar, float* M_in,
+                          float* M_out, int32_t V, int32_t D, int32_t ld,
+                          void* workspace, size_t workspace_bytes, int64_t* stats,
+                          void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -407,6 +407,64 @@ int w2v_step_batch(int32_t B, int32_t N, int32_t K, const int32_t* targets,
   return ok();
 }
 
+size_t w2v_step_batch_sorted_workspace_bytes(int32_t B, int32_t N, int32_t K,
+                                             int32_t V, int32_t ld) {
+  if (B < 0 || N < 0 || K < 0 || V <= 0 || ld <= 0) return 0;
+  return sorted_step_workspace_bytes(B, N, K, V, ld);
+}
+
+int w2v_step_batch_sorted(int32_t B, int32_t N, int32_t K, const int32_t* targets,
+                          const int32_t* contexts, const int32_t* negatives,
+                          const float* alpha, float alpha_scalar, float* M_in,
+                          float* M_out, int32_t V, int32_t D, int32_t ld,
+                          void* workspace, size_t workspace_bytes, int64_t* stats,
+                          void* stream) {
+  if (B < 0) return fail(W2V_EINVAL, "B must be >= 0");
+  if (N < 0 || N > W2V_MAX_BATCH_INPUTS)
+    return failf(W2V_EINVAL, "N must be in [0, %d]", W2V_MAX_BATCH_INPUTS);
+  if (K < 0 || K > W2V_MAX_NEGATIVE)
+    return failf(W2V_EINVAL, "K must be in [0, %d]", W2V_MAX_NEGATIVE);
+  if ((int64_t)B * (N + K + 1) > INT32_MAX)
+    return fail(W2V_EINVAL, "B * (N + K + 1) must fit in int32");
+  int rc = check_matrices(M_in, M_out, V, D, ld);
+  if (rc != W2V_OK) return rc;
+  if (B > 0 && targets == nullptr) return fail(W2V_EINVAL, "targets is NULL");
+  if (B > 0 && N > 0 && contexts == nullptr)
+    return fail(W2V_EINVAL, "contexts is NULL");
+  if (B > 0 && K > 0 && negatives == nullptr)
+    return fail(W2V_EINVAL, "negatives is NULL");
+  const size_t need = w2v_step_batch_sorted_workspace_bytes(B, N, K, V, ld);
+  if (need == 0) return fail(W2V_EHIP, "sort size query failed");
+  if (workspace == nullptr || workspace_bytes < need)
+    return failf(W2V_EINVAL, "workspace must hold %zu bytes", need);
+  if (((uintptr_t)workspace & 255u) != 0)
+    return fail(W2V_EINVAL, "workspace must be 256-byte aligned");
+  const int C = columns_for(D);
+  const int nmax = inputs_cap_for(N > 0 ? N : 1);
+  if (C == 0 || nmax == 0 || !sorted_step_supported(C, nmax))
+    return failf(W2V_EUNSUPPORTED, "no compiled kernel for D=%d N=%d", D, N);
+  if (B == 0 || N == 0) return ok();
+
+  SortedStepArgs a{};
+  a.B = B;
+  a.N = N;
+  a.K = K;
+  a.targets = targets;
+  a.contexts = contexts;
+  a.negatives = negatives;
+  a.alpha = alpha;
+  a.alpha_scalar = alpha_scalar;
+  a.M_in = M_in;
+  a.M_out = M_out;
+  a.V = V;
+  a.D = D;
+  a.ld = ld;
+  a.stats = stats;
+  hipError_t e = launch_step_sorted(C, nmax, a, workspace, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "sorted step launch");
+  return ok();
+}
+
 size_t w2v_build_vocab_workspace_bytes(int32_t V_raw) {
   if (V_raw <= 0) return 0;
   return vocab_workspace_bytes(V_raw);

@@ -57,6 +57,30 @@ struct StepArgs {
   int64_t* stats;
 };
 
+// Sorted snapshot batch: the snapshot batch's inputs plus the staging rows
+// and sort keys it writes (step_sorted.hip sets the workspace pointers).
+struct SortedStepArgs {
+  int32_t B, N, K;
+  const int32_t* targets;
+  const int32_t* contexts;
+  const int32_t* negatives;
+  const float* alpha;      // NULL: alpha_scalar
+  float alpha_scalar;
+  float* M_in;
+  float* M_out;
+  int32_t V, D;
+  int64_t ld;
+  int64_t* stats;
+  float* stage_in;         // [B][N][ld] updates of the distinct input rows
+  float* stage_out;        // [B][K+1][ld] updates of the output rows
+  uint32_t* key_in;        // [B][N] sort key of each staging row: the M_in
+                           // row id, 2V if unused
+  int32_t* val_in;         // [B][N] staging index
+  uint32_t* key_out;       // [B][K+1] V + the M_out row id, 2V if unused
+  int32_t* val_out;        // [B][K+1] staging index (counted from stage_in)
+  int64_t out_base;        // staging index of stage_out's first row
+};
+
 // Workgroups of one wavefront of `kernel` resident per CU with `dyn_lds`
 // bytes of dynamic LDS (0 on a failed query).
 int resident_blocks_per_cu(const void* kernel, size_t dyn_lds);
@@ -72,6 +96,12 @@ hipError_t launch_part_fold(const EpochArgs& a, hipStream_t s);
 hipError_t launch_step(int C, int nmax, const StepArgs& a, int grid,
                        hipStream_t s);
 bool train_shape_supported(int C, int nmax);
+// Sorted snapshot batch (step_sorted.hip).
+size_t sorted_step_workspace_bytes(int32_t B, int32_t N, int32_t K, int32_t V,
+                                   int32_t ld);
+bool sorted_step_supported(int C, int nmax);
+hipError_t launch_step_sorted(int C, int nmax, SortedStepArgs a, void* workspace,
+                              hipStream_t s);
 int columns_for(int D);      // compiled C for a row length, 0 if none
 int inputs_cap_for(int n);   // compiled nmax for n input words, 0 if none
 int train_blocks_per_cu(int C, int nmax, int K);

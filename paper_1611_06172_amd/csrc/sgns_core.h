@@ -266,6 +266,10 @@ struct NoPendingRows {
   __device__ __forceinline__ bool defer(int, int, const float (&)[C]) const {
     return false;
   }
+  template <int C>
+  __device__ __forceinline__ bool defer_out(int, int, const float (&)[C]) const {
+    return false;
+  }
 };
 
 // rows: [slots][64 C] floats in LDS, the updates a wavefront has made to an
@@ -303,6 +307,41 @@ struct PendingRows {
 #pragma unroll
       for (int c = 0; c < C; ++c) p[kWave * c] = g[c];
     }
+    return true;
+  }
+  template <int C>
+  __device__ __forceinline__ bool defer_out(int, int, const float (&)[C]) const {
+    return false;
+  }
+};
+
+// Updates written out instead of applied (sorted snapshot batches): the
+// update of distinct input i goes to row i of `in`, that of output column k
+// to row k of `out` (row stride ld; columns past D are not written).
+struct StagedRows {
+  float* in;
+  float* out;
+  int64_t ld;
+  int D;
+
+  template <int C>
+  __device__ __forceinline__ void add_pending(int, int, float (&)[C]) const {}
+  template <int C>
+  __device__ __forceinline__ void put(float* row, int lane,
+                                      const float (&g)[C]) const {
+#pragma unroll
+    for (int c = 0; c < C; ++c)
+      if (lane + kWave * c < D) row[lane + kWave * c] = g[c];
+  }
+  template <int C>
+  __device__ __forceinline__ bool defer(int i, int lane, const float (&g)[C]) const {
+    put<C>(in + i * ld, lane, g);
+    return true;
+  }
+  template <int C>
+  __device__ __forceinline__ bool defer_out(int k, int lane,
+                                            const float (&g)[C]) const {
+    put<C>(out + k * ld, lane, g);
     return true;
   }
 };
@@ -431,7 +470,8 @@ __device__ __forceinline__ void run_minibatch(
             for (int c = 0; c < C; ++c) g[c] = fmaf(e, a[i][c], g[c]);
           }
         }
-        update(1, Wout, uniform_int(mb.out[k]), o[kk], g);
+        if (!pend.template defer_out<C>(k, lane, g))
+          update(1, Wout, uniform_int(mb.out[k]), o[kk], g);
       }
     }
 

@@ -81,6 +81,10 @@ def lib():
         _i32, _i32, _i32, _vp, _vp, _vp, _vp, _f32, _vp, _vp, _i32, _i32, _i32,
         _vp, ctypes.c_size_t, _vp, _vp]
     L.w2v_step_batch.restype = ctypes.c_int
+    L.w2v_step_batch_sorted_workspace_bytes.argtypes = [_i32, _i32, _i32, _i32, _i32]
+    L.w2v_step_batch_sorted_workspace_bytes.restype = ctypes.c_size_t
+    L.w2v_step_batch_sorted.argtypes = L.w2v_step_batch.argtypes
+    L.w2v_step_batch_sorted.restype = ctypes.c_int
     _lib = L
     return L
 
@@ -303,10 +307,16 @@ def alloc_workspace(V: int, ld: int, device="cuda"):
     return torch.empty(n, dtype=torch.uint8, device=device)
 
 
+def step_batch_sorted_workspace_bytes(B: int, N: int, K: int, V: int, ld: int) -> int:
+    return int(lib().w2v_step_batch_sorted_workspace_bytes(B, N, K, V, ld))
+
+
 def step_batch(targets, contexts, negatives, M_in, M_out, alpha=0.025, *,
                D: Optional[int] = None, workspace=None, stats=None,
-               stream=None):
-    """One snapshot batch of B minibatches; updates M_in, M_out in place."""
+               stream=None, sorted: bool = False):
+    """One snapshot batch of B minibatches; updates M_in, M_out in place.
+    sorted: sum each row's updates in a fixed order (w2v_step_batch_sorted:
+    the same bits on every run) instead of with fp64 atomics."""
     import torch
     _dev(targets, torch.int32, "targets", 1)
     _dev(contexts, torch.int32, "contexts", 2)
@@ -326,10 +336,19 @@ def step_batch(targets, contexts, negatives, M_in, M_out, alpha=0.025, *,
     else:
         a_ptr, a_s = None, float(alpha)
     if workspace is None:
-        workspace = alloc_workspace(V, ld, M_in.device)
+        if sorted:
+            n = step_batch_sorted_workspace_bytes(B, N, K, V, ld)
+            if n == 0:
+                _check(lib().w2v_step_batch_sorted(
+                    B, N, K, None, None, None, None, 0.0, None, None, V, D, ld,
+                    None, 0, None, None))
+            workspace = torch.empty(n, dtype=torch.uint8, device=M_in.device)
+        else:
+            workspace = alloc_workspace(V, ld, M_in.device)
     if stats is not None:
         _dev(stats, torch.int64, "stats", 1)
-    _check(lib().w2v_step_batch(
+    entry = lib().w2v_step_batch_sorted if sorted else lib().w2v_step_batch
+    _check(entry(
         B, N, K, _ptr(targets), _ptr(contexts), _ptr(negatives), a_ptr, a_s,
         _ptr(M_in), _ptr(M_out), V, D, ld, _ptr(workspace),
         workspace.numel() * workspace.element_size(), _ptr(stats),

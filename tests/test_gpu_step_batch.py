@@ -20,7 +20,8 @@ pytestmark = pytest.mark.gpu
 TOL = 1e-5
 
 
-def check(targets, contexts, negatives, M_in, M_out, alpha, D=None, expect_skip=0):
+def check(targets, contexts, negatives, M_in, M_out, alpha, D=None, expect_skip=0,
+          sorted=False):
     import torch
     V, ld = M_in.shape
     D = ld if D is None else D
@@ -30,7 +31,7 @@ def check(targets, contexts, negatives, M_in, M_out, alpha, D=None, expect_skip=
     a = to_dev(alpha) if np.ndim(alpha) else alpha
     stats = torch.zeros(4, dtype=torch.int64, device="cuda")
     w2v.step_batch(to_dev(targets), to_dev(contexts), to_dev(negatives), gi, go,
-                   a, D=D, stats=stats)
+                   a, D=D, stats=stats, sorted=sorted)
     torch.cuda.synchronize()
     gi, go = gi.cpu().numpy(), go.cpu().numpy()
     for name, g, o, S, M0 in (("M_in", gi, Mi_o, S_in, M_in),

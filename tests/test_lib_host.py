@@ -182,3 +182,28 @@ def test_build_vocab_rejects(over, needle):
 def test_pending_slots_rejects(args, needle):
     assert w2v.lib().w2v_pending_slots(*args) == w2v.EINVAL
     assert needle in w2v.lib().w2v_last_error().decode()
+
+
+def sorted_step(**over):
+    args = dict(B=4, N=2, K=1, t=FAKE, c=FAKE, n=FAKE, alpha=None, a_s=0.0,
+                Mi=FAKE, Mo=FAKE + 0x1000, V=10, D=8, ld=8, ws=0x100000,
+                ws_bytes=1 << 30, stats=None, stream=None)
+    args.update(over)
+    return w2v.lib().w2v_step_batch_sorted(*args.values())
+
+
+@pytest.mark.parametrize("over,needle", [
+    (dict(B=-1), "B"), (dict(N=33), "N"), (dict(K=65), "K"),
+    (dict(B=1 << 30, K=64), "int32"), (dict(t=None), "targets"),
+    (dict(c=None), "contexts"), (dict(n=None), "negatives"), (dict(D=9), "D"),
+])
+def test_step_batch_sorted_rejects(over, needle):
+    assert sorted_step(**over) == w2v.EINVAL
+    assert needle in w2v.lib().w2v_last_error().decode()
+
+
+def test_step_batch_sorted_workspace_rejects_invalid_shapes():
+    L = w2v.lib()
+    for args in ((-1, 2, 1, 10, 8), (4, -1, 1, 10, 8), (4, 2, -1, 10, 8),
+                 (4, 2, 1, 0, 8), (4, 2, 1, 10, 0)):
+        assert L.w2v_step_batch_sorted_workspace_bytes(*args) == 0
