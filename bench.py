@@ -92,6 +92,13 @@ def main():
                     help="run a 1 GiB device copy first (counter calibration)")
     ap.add_argument("--cpu-sample-tokens", type=int, default=2_000_000)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--workload", choices=["large-vocab", "kernel-test"],
+                    default="large-vocab",
+                    help="large-vocab: the HogBatch epoch (the measured path); "
+                         "kernel-test: one snapshot batch of 65,536 minibatches "
+                         "(w2v_step_batch)")
+    ap.add_argument("--step-mode", choices=["sorted", "atomic"], default="sorted",
+                    help="kernel-test: w2v_step_batch_sorted or w2v_step_batch")
     ap.add_argument("--traffic-json",
                     default=os.path.join(ROOT, "profiles", "k_epoch_traffic.json"))
     args = ap.parse_args()
@@ -100,6 +107,10 @@ def main():
         print("bench.py measures one GPU only: this build has no multi-GPU path "
               "(see the sharding design); run with --gpus 1", file=sys.stderr)
         sys.exit(2)
+
+    if args.workload == "kernel-test":
+        kernel_test(args)
+        return
 
     import numpy as np
     import torch
@@ -256,6 +267,85 @@ def main():
             "sample": (f"first {n_s} tokens of the same corpus as a 1-epoch run "
                        f"({n_o} minibatches, same tables and initial M_in), "
                        f"single-threaded fp64 oracle, {c_dt:.1f}s; host has "
+                       f"{os.cpu_count()} logical CPUs"),
+        }
+    print(json.dumps(result), flush=True)
+
+
+def kernel_test(args):
+    """One snapshot batch per step on the kernel-test configuration: B =
+    65,536 minibatches of 1 target, N = 10 inputs and K = 5 negatives, i.i.d.
+    Zipf(1.0) ids over V = 100,000, D = 300 (rows padded to 320), M ~ N(0,
+    0.1^2), alpha 0.025."""
+    import numpy as np
+    import torch
+
+    from paper_1611_06172_amd import inputs, w2v
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    B, N, K, V, D = 65536, 10, 5, 100_000, 300
+    t, c, n = inputs.kernel_batch(B, N, K, V, 1.0, 3)
+    Mi0 = inputs.init_matrix(V, D, "normal", 4)
+    Mo0 = inputs.init_matrix(V, D, "normal", 104)
+    M_in = w2v.alloc_matrix(V, D, dev, torch.from_numpy(Mi0))
+    M_out = w2v.alloc_matrix(V, D, dev, torch.from_numpy(Mo0))
+    T, C, Ng = (torch.from_numpy(x).to(dev) for x in (t, c, n))
+    srt = args.step_mode == "sorted"
+    ws = w2v.step_batch(T, C, Ng, M_in, M_out, 0.025, D=D, sorted=srt)  # allocates
+    for _ in range(max(args.warmup, 0)):
+        w2v.step_batch(T, C, Ng, M_in, M_out, 0.025, D=D, workspace=ws, sorted=srt)
+    steps = max(args.steps, 1) * 20   # a batch takes about a millisecond
+    stream = torch.cuda.current_stream()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(steps)]
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for i in range(steps):
+        evs[i][0].record(stream)
+        w2v.step_batch(T, C, Ng, M_in, M_out, 0.025, D=D, workspace=ws, sorted=srt)
+        evs[i][1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_start
+    call_ms = [a.elapsed_time(b) for a, b in evs]
+    print(f"[bench] timed {steps} batches in {wall:.3f}s; median call "
+          f"{float(np.median(call_ms)):.3f} ms", file=sys.stderr, flush=True)
+    # Algorithmic bytes: every minibatch gathers and writes back its N + K + 1
+    # rows (8 D bytes per row).
+    alg_bytes = 8.0 * D * B * (N + K + 1)
+    call_s = float(np.mean(call_ms)) / 1e3
+    achieved = alg_bytes / call_s / 1e9
+    entry = "w2v_step_batch_sorted" if srt else "w2v_step_batch"
+    result = {
+        "metric": "Mminibatches/sec, snapshot batch (kernel test)",
+        "value": round(B / (wall / steps) / 1e6, 3),
+        "unit": "Mminibatches/s",
+        "n_gpus": 1, "steps": steps, "warmup": args.warmup,
+        "ms_per_step": round(wall * 1e3 / steps, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f32", "data": "synthetic",
+        "config": {"workload": f"kernel-test snapshot batch ({entry}): B={B}, N={N}, "
+                               f"K={K}, i.i.d. Zipf(1.0) ids over V={V}, D={D}, "
+                               f"alpha 0.025",
+                   "B": B, "N": N, "K": K, "V": V, "D": D, "ld": M_in.stride(0),
+                   "workspace_bytes": int(ws.numel())},
+        "roofline": {"bound": "hbm", "kernel": entry + " (all launches of one call)",
+                     "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "traffic": None, "alg_bytes_per_launch": alg_bytes,
+                     "kernel_ms": round(call_s * 1e3, 4)},
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        bs = B
+        c0 = time.perf_counter()
+        oracle.step_batch(t[:bs], c[:bs], n[:bs], Mi0, Mo0, 0.025, D=D, with_scale=False)
+        c_dt = time.perf_counter() - c0
+        result["cpu_baseline"] = {
+            "value": round(bs / c_dt / 1e6, 5), "unit": "Mminibatches/s",
+            "cores": 1, "kind": "oracle",
+            "sample": (f"the whole batch ({bs} minibatches), single-threaded fp64 "
+                       f"oracle snapshot batch, {c_dt:.1f}s; host has "
                        f"{os.cpu_count()} logical CPUs"),
         }
     print(json.dumps(result), flush=True)
