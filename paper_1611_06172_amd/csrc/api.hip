@@ -263,6 +263,7 @@ int w2v_train_epoch(const int32_t* corpus, int64_t T, int64_t pos_begin,
                      ? 0
                      : train_pending_slots(C, nmax, K);
   a.pend_from = pending_from(hot_rows, split_rows);
+  a.target_batch = (pairwise || grouped) ? 64 : train_target_batch(C, nmax, K);
 
   int64_t grid = max_inflight;
   if (grid == 0) {

@@ -92,7 +92,8 @@ __global__ __launch_bounds__(kWave) void k_epoch(EpochArgs a) {
   const int lane = threadIdx.x;
   const int K = a.K;
   const bool want_loss = a.loss != nullptr;
-  float* const slot_rows = reinterpret_cast<float*>(negs_lds + kWave * (K > 0 ? K : 1));
+  const int TB = kExport ? kWave : a.target_batch;
+  float* const slot_rows = reinterpret_cast<float*>(negs_lds + TB * (K > 0 ? K : 1));
   const int nslots = kExport ? 0 : a.pend_slots;
   int slot_id = -1, slot_t = 0;
   const RowTiers<C, false> io{a.part, a.split_rows, a.hot_rows, a.ld, a.D, lane};
@@ -116,9 +117,9 @@ __global__ __launch_bounds__(kWave) void k_epoch(EpochArgs a) {
     raw += len;
     const int n_ret = keep_and_compact<kExport>(a, sb, len, lane, sl, rejected);
 
-    for (int q0 = 0; q0 < n_ret; q0 += kWave) {
-      form_targets<kExport>(a, sb, q0, n_ret, lane, sl, tb, negs_lds);
-      const int cnt = min(kWave, n_ret - q0);
+    for (int q0 = 0; q0 < n_ret; q0 += TB) {
+      form_targets<kExport>(a, sb, q0, n_ret, lane, sl, tb, negs_lds, TB);
+      const int cnt = min(TB, n_ret - q0);
       for (int j = 0; j < cnt; ++j) {
         const int n = uniform_int(tb.n[j]);
         if (n == 0) continue;
@@ -432,8 +433,8 @@ int resident_blocks_per_cu(const void* kernel, size_t dyn_lds) {
   return blocks < by_lds ? blocks : by_lds;
 }
 
-static size_t negatives_lds(int K) {
-  return sizeof(int32_t) * (size_t)kWave * (size_t)(K > 0 ? K : 1);
+static size_t negatives_lds(int K, int batch = kWave) {
+  return sizeof(int32_t) * (size_t)batch * (size_t)(K > 0 ? K : 1);
 }
 
 static size_t epoch_dyn_lds(const EpochArgs& a) {
@@ -444,22 +445,33 @@ static size_t slot_bytes(int C) { return sizeof(float) * (size_t)kWave * C; }
 
 constexpr int kMaxPendingSlots = 16;
 
+int train_target_batch(int C, int nmax, int K) {
+  EpochKernel k = train_kernel_for(C, nmax, K);
+  if (k == nullptr) return kWave;
+  const void* f = reinterpret_cast<const void*>(k);
+  const int best = resident_blocks_per_cu(f, negatives_lds(K, 8));
+  int tb = kWave;
+  while (tb > 8 && resident_blocks_per_cu(f, negatives_lds(K, tb)) < best) tb /= 2;
+  return tb;
+}
+
 int train_pending_slots(int C, int nmax, int K) {
   EpochKernel k = train_kernel_for(C, nmax, K);
   if (k == nullptr) return 0;
   const void* f = reinterpret_cast<const void*>(k);
-  const int base = resident_blocks_per_cu(f, negatives_lds(K));
+  const size_t negs = negatives_lds(K, train_target_batch(C, nmax, K));
+  const int base = resident_blocks_per_cu(f, negs);
   if (base <= 0) return 0;
   for (int n = kMaxPendingSlots; n >= 2; --n)
-    if (resident_blocks_per_cu(f, negatives_lds(K) + n * slot_bytes(C)) >= base)
-      return n;
+    if (resident_blocks_per_cu(f, negs + n * slot_bytes(C)) >= base) return n;
   return 0;
 }
 
 int train_blocks_per_cu(int C, int nmax, int K) {
   EpochKernel k = train_kernel_for(C, nmax, K);
   if (k == nullptr) return 0;
-  return resident_blocks_per_cu(reinterpret_cast<const void*>(k), negatives_lds(K));
+  return resident_blocks_per_cu(reinterpret_cast<const void*>(k),
+                                negatives_lds(K, train_target_batch(C, nmax, K)));
 }
 
 hipError_t launch_train(int C, int nmax, const EpochArgs& a, int grid,
@@ -467,7 +479,8 @@ hipError_t launch_train(int C, int nmax, const EpochArgs& a, int grid,
   EpochKernel k = train_kernel_for(C, nmax, a.K);
   if (k == nullptr) return hipErrorInvalidValue;
   hipLaunchKernelGGL(k, dim3(grid), dim3(kWave),
-                     epoch_dyn_lds(a) + a.pend_slots * slot_bytes(C), s, a);
+                     negatives_lds(a.K, a.target_batch) + a.pend_slots * slot_bytes(C),
+                     s, a);
   return hipGetLastError();
 }
 

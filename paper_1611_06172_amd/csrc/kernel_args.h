@@ -32,6 +32,8 @@ struct EpochArgs {
   float* part;             // [2][split_rows][kSplitParts][ld] partial rows
   int32_t pend_slots;      // LDS pending input-row slots per wavefront (0: none)
   int32_t pend_from;       // ids below this never take a pending slot
+  int32_t target_batch;    // targets k_epoch forms at once (<= 64; its
+                           // negatives take target_batch * K ints of LDS)
   // export outputs (minibatch export only)
   int32_t* out_targets;
   int32_t* out_ctx;
@@ -108,6 +110,9 @@ int train_blocks_per_cu(int C, int nmax, int K);
 // Pending input-row slots that fit beside the training kernel's LDS without
 // lowering its occupancy (0 if fewer than two fit).
 int train_pending_slots(int C, int nmax, int K);
+// Targets the training kernel forms at once: 64, or fewer where the
+// negatives of 64 targets would cost LDS residency (large K).
+int train_target_batch(int C, int nmax, int K);
 // HogBatch with negatives shared by groups of targets: omax = compiled
 // capacity of output columns (G + K).
 int group_outputs_cap_for(int n);

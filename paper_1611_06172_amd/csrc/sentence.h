@@ -5,7 +5,7 @@
 //  * keep_and_compact: reads a sentence's raw ids, decides subsampling per
 //    position (Philox word 0 against the keep threshold) and compacts the
 //    kept words into LDS with a ballot prefix count.
-//  * form_targets: forms 64 targets lane-parallel: window half-width
+//  * form_targets: forms up to 64 targets lane-parallel: window half-width
 //    (word 1), the K shared negatives (words 2.., one table read each), the
 //    decayed learning rate, and whether a negative id is out of range.
 #pragma once
@@ -72,19 +72,20 @@ __device__ __forceinline__ int keep_and_compact(const EpochArgs& a, int64_t sb,
   return n_ret;
 }
 
-// Forms targets q0 + lane (lane < 64, q0 + lane < n_ret) into tb and their
-// negatives into negs[lane * K + k]. The export variant also writes the
-// minibatches out.
+// Forms targets q0 + lane (lane < n_batch <= 64, q0 + lane < n_ret) into tb
+// and their negatives into negs[lane * K + k]. The export variant also
+// writes the minibatches out.
 template <bool kExport>
 __device__ __forceinline__ void form_targets(const EpochArgs& a, int64_t sb,
                                              int q0, int n_ret, int lane,
                                              const SentenceLds& sl,
-                                             TargetBatch& tb, int32_t* negs) {
+                                             TargetBatch& tb, int32_t* negs,
+                                             int n_batch = kWave) {
   const uint64_t e = (uint64_t)a.epoch;
   const int K = a.K;
   const int w = a.w;
   const int q = q0 + lane;
-  if (q < n_ret) {
+  if (q < n_ret && lane < n_batch) {
     const int64_t p = sb + sl.ret_off[q];
     const int t = sl.ret_id[q];
     U64x4 blk = stream_block(a.seed, (uint64_t)p, e, 0);
