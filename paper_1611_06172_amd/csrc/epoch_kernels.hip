@@ -14,6 +14,9 @@
 // reductions. The export variant stops after step 2 and writes the
 // minibatches out.
 #include <climits>
+#include <map>
+#include <mutex>
+#include <tuple>
 
 #include "group_core.h"
 #include "kernel_args.h"
@@ -445,34 +448,52 @@ static size_t slot_bytes(int C) { return sizeof(float) * (size_t)kWave * C; }
 
 constexpr int kMaxPendingSlots = 16;
 
-int train_target_batch(int C, int nmax, int K) {
+// Shape of the training launch for (C, nmax, K) on the current device:
+// targets formed at once, pending slots and resident workgroups per CU.
+// Computed from occupancy queries once per device and shape.
+struct TrainShape {
+  int target_batch, pending_slots, blocks_per_cu;
+};
+
+static TrainShape compute_train_shape(int C, int nmax, int K) {
+  TrainShape t{kWave, 0, 0};
   EpochKernel k = train_kernel_for(C, nmax, K);
-  if (k == nullptr) return kWave;
+  if (k == nullptr) return t;
   const void* f = reinterpret_cast<const void*>(k);
   const int best = resident_blocks_per_cu(f, negatives_lds(K, 8));
-  int tb = kWave;
-  while (tb > 8 && resident_blocks_per_cu(f, negatives_lds(K, tb)) < best) tb /= 2;
-  return tb;
-}
-
-int train_pending_slots(int C, int nmax, int K) {
-  EpochKernel k = train_kernel_for(C, nmax, K);
-  if (k == nullptr) return 0;
-  const void* f = reinterpret_cast<const void*>(k);
-  const size_t negs = negatives_lds(K, train_target_batch(C, nmax, K));
-  const int base = resident_blocks_per_cu(f, negs);
-  if (base <= 0) return 0;
+  while (t.target_batch > 8 &&
+         resident_blocks_per_cu(f, negatives_lds(K, t.target_batch)) < best)
+    t.target_batch /= 2;
+  const size_t negs = negatives_lds(K, t.target_batch);
+  t.blocks_per_cu = resident_blocks_per_cu(f, negs);
+  if (t.blocks_per_cu <= 0) return t;
   for (int n = kMaxPendingSlots; n >= 2; --n)
-    if (resident_blocks_per_cu(f, negs + n * slot_bytes(C)) >= base) return n;
-  return 0;
+    if (resident_blocks_per_cu(f, negs + n * slot_bytes(C)) >= t.blocks_per_cu) {
+      t.pending_slots = n;
+      break;
+    }
+  return t;
 }
 
-int train_blocks_per_cu(int C, int nmax, int K) {
-  EpochKernel k = train_kernel_for(C, nmax, K);
-  if (k == nullptr) return 0;
-  return resident_blocks_per_cu(reinterpret_cast<const void*>(k),
-                                negatives_lds(K, train_target_batch(C, nmax, K)));
+static TrainShape train_shape(int C, int nmax, int K) {
+  static std::mutex mu;
+  static std::map<std::tuple<int, int, int, int>, TrainShape> cache;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return compute_train_shape(C, nmax, K);
+  const auto key = std::make_tuple(dev, C, nmax, K);
+  std::lock_guard<std::mutex> lock(mu);
+  auto it = cache.find(key);
+  if (it != cache.end()) return it->second;
+  const TrainShape t = compute_train_shape(C, nmax, K);
+  if (t.blocks_per_cu > 0) cache[key] = t;  // failed queries are retried
+  return t;
 }
+
+int train_target_batch(int C, int nmax, int K) { return train_shape(C, nmax, K).target_batch; }
+
+int train_pending_slots(int C, int nmax, int K) { return train_shape(C, nmax, K).pending_slots; }
+
+int train_blocks_per_cu(int C, int nmax, int K) { return train_shape(C, nmax, K).blocks_per_cu; }
 
 hipError_t launch_train(int C, int nmax, const EpochArgs& a, int grid,
                         hipStream_t s) {
