@@ -206,6 +206,10 @@ def main():
     achieved = alg_bytes / avg_kern_s / 1e9
     traffic = (measured_traffic(args.traffic_json, 1.0)
                if args.algorithm == "hogbatch" and args.group == 1 else None)
+    # Grouped negatives move one set of output rows per group and each
+    # distinct input row once per group; the kernel keeps no count of those,
+    # so the per-target byte count above would overstate the work.
+    grouped = args.group > 1
 
     result = {
         "metric": METRIC,
@@ -237,15 +241,18 @@ def main():
             "bound": "hbm",
             "kernel": ("k_epoch_pairwise" if args.algorithm == "pairwise" else
                        "k_epoch_grouped" if args.group > 1 else "k_epoch"),
-            "achieved": round(achieved, 1),
+            "achieved": None if grouped else round(achieved, 1),
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
-            "frac": round(achieved / HBM_PEAK_GBS, 4),
+            "frac": None if grouped else round(achieved / HBM_PEAK_GBS, 4),
             "traffic": traffic,
-            "alg_bytes_per_launch": alg_bytes,
+            "alg_bytes_per_launch": None if grouped else alg_bytes,
             "kernel_ms": round(avg_kern_s * 1e3, 3),
         },
     }
+    if grouped:
+        result["roofline"]["note"] = ("grouped negatives: no per-group count of the "
+                                      "rows moved is kept, so no algorithmic bytes")
 
     if not args.no_cpu_baseline:
         import oracle
