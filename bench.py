@@ -92,11 +92,12 @@ def main():
                     help="run a 1 GiB device copy first (counter calibration)")
     ap.add_argument("--cpu-sample-tokens", type=int, default=2_000_000)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--workload", choices=["large-vocab", "kernel-test"],
+    ap.add_argument("--workload", choices=["large-vocab", "kernel-test", "vocab"],
                     default="large-vocab",
                     help="large-vocab: the HogBatch epoch (the measured path); "
                          "kernel-test: one snapshot batch of 65,536 minibatches "
-                         "(w2v_step_batch)")
+                         "(w2v_step_batch); vocab: the vocabulary pipeline "
+                         "(w2v_build_vocab) over --tokens raw ids")
     ap.add_argument("--step-mode", choices=["sorted", "atomic"], default="sorted",
                     help="kernel-test: w2v_step_batch_sorted or w2v_step_batch")
     ap.add_argument("--traffic-json",
@@ -110,6 +111,9 @@ def main():
 
     if args.workload == "kernel-test":
         kernel_test(args)
+        return
+    if args.workload == "vocab":
+        vocab_bench(args)
         return
 
     import numpy as np
@@ -354,6 +358,92 @@ def kernel_test(args):
             "sample": (f"the whole batch ({bs} minibatches), single-threaded fp64 "
                        f"oracle snapshot batch, {c_dt:.1f}s; host has "
                        f"{os.cpu_count()} logical CPUs"),
+        }
+    print(json.dumps(result), flush=True)
+
+
+def vocab_bench(args):
+    """The vocabulary pipeline on --tokens raw ids: i.i.d. Zipf(1.07) over
+    2,000,000 raw words whose ids are shuffled (so raw order is not frequency
+    order); count, rank (ties by raw id), cut at min_count 5, rewrite the
+    corpus in ranked ids."""
+    import numpy as np
+    import torch
+
+    from paper_1611_06172_amd import inputs, w2v
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    T, V_raw, min_count = int(args.tokens), 2_000_000, 5
+    g = torch.Generator(device=dev)
+    g.manual_seed(11)
+    perm = torch.randperm(V_raw, generator=g, device=dev).to(torch.int32)
+    raw = perm[inputs.zipf_corpus_device(T, V_raw, 1.07, 6, dev).long()]
+    del perm
+    L = w2v.lib()
+    ranked = torch.empty(V_raw, dtype=torch.int64, device=dev)
+    rank_of = torch.empty(V_raw, dtype=torch.int32, device=dev)
+    v_kept = torch.empty(1, dtype=torch.int32, device=dev)
+    corpus = torch.empty(T, dtype=torch.int32, device=dev)
+    ws = torch.empty(int(L.w2v_build_vocab_workspace_bytes(V_raw)), dtype=torch.uint8,
+                     device=dev)
+    stream = torch.cuda.current_stream()
+
+    def call():
+        rc = L.w2v_build_vocab(w2v._ptr(raw), T, V_raw, min_count, w2v._ptr(ranked),
+                               w2v._ptr(rank_of), w2v._ptr(v_kept), w2v._ptr(corpus),
+                               w2v._ptr(ws), ws.numel(), w2v._stream(stream))
+        w2v._check(rc)
+
+    for _ in range(max(args.warmup, 0)):
+        call()
+    steps = max(args.steps, 1)
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(steps)]
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for i in range(steps):
+        evs[i][0].record(stream)
+        call()
+        evs[i][1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_start
+    call_ms = [a.elapsed_time(b) for a, b in evs]
+    V = int(v_kept.item())
+    print(f"[bench] timed {steps} calls in {wall:.3f}s; per call "
+          f"{[round(x, 2) for x in call_ms]} ms; V = {V}", file=sys.stderr, flush=True)
+    # Algorithmic bytes: the raw ids are read twice (count, rewrite) and the
+    # rewritten corpus written once; the per-word arrays are negligible.
+    alg_bytes = 12.0 * T
+    call_s = float(np.mean(call_ms)) / 1e3
+    achieved = alg_bytes / call_s / 1e9
+    result = {
+        "metric": "Mtokens/sec, vocabulary pipeline (count, rank, cut, rewrite)",
+        "value": round(T / (wall / steps) / 1e6, 1), "unit": "Mtokens/s",
+        "n_gpus": 1, "steps": steps, "warmup": args.warmup,
+        "ms_per_step": round(wall * 1e3 / steps, 3), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "int32/int64",
+        "data": "synthetic",
+        "config": {"workload": f"vocabulary of {T} i.i.d. Zipf(1.07) raw ids over "
+                               f"{V_raw} shuffled raw words, min_count {min_count}",
+                   "T": T, "V_raw": V_raw, "min_count": min_count, "V_kept": V},
+        "roofline": {"bound": "hbm", "kernel": "w2v_build_vocab (all launches of one call)",
+                     "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                     "alg_bytes_per_launch": alg_bytes, "kernel_ms": round(call_s * 1e3, 3)},
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        n_s = min(T, 100_000_000)
+        sample = raw[:n_s].cpu().numpy()
+        c0 = time.perf_counter()
+        oracle.build_vocab(sample, V_raw, min_count)
+        c_dt = time.perf_counter() - c0
+        result["cpu_baseline"] = {
+            "value": round(n_s / c_dt / 1e6, 2), "unit": "Mtokens/s", "cores": 1,
+            "kind": "oracle",
+            "sample": (f"first {n_s} raw ids, numpy bincount + stable argsort oracle, "
+                       f"{c_dt:.1f}s; host has {os.cpu_count()} logical CPUs"),
         }
     print(json.dumps(result), flush=True)
 
