@@ -13,6 +13,7 @@ stream, and the CPU oracle's rate on a bounded sample of the same workload.
 """
 import argparse
 import hashlib
+import re
 import json
 import os
 import sys
@@ -33,10 +34,15 @@ WORKLOAD_NAME = {"hogbatch": "HogBatch",
 
 
 def kernel_hash():
+    """Hash of the epoch kernel's sources with comments and blank space
+    removed, so that editing a comment does not void a counter summary."""
     h = hashlib.sha256()
     for name in KERNEL_SOURCES:
-        with open(os.path.join(ROOT, "paper_1611_06172_amd", "csrc", name), "rb") as f:
-            h.update(f.read())
+        with open(os.path.join(ROOT, "paper_1611_06172_amd", "csrc", name)) as f:
+            text = f.read()
+        text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", " ", text)
+        h.update(" ".join(text.split()).encode())
     return h.hexdigest()[:16]
 
 

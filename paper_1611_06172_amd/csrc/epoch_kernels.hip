@@ -3,13 +3,14 @@
 // One wavefront owns one sentence at a time (a persistent grid strides over
 // the sentences of the range). For its sentence it
 //   1. decides subsampling and compacts the kept words (sentence.h);
-//   2. forms 64 targets at a time lane-parallel (sentence.h);
+//   2. forms up to 64 targets at a time lane-parallel (sentence.h; fewer
+//      where their negatives would cost LDS residency);
 //   3. runs those targets' minibatches in sentence order through the fused
 //      minibatch (sgns_core.h), so every minibatch of a sentence sees the
 //      updates of the ones before it, while minibatches of different
 //      sentences interleave without locks (Hogwild, Sec. 1.1). The updates
-//      of input rows collect in a few LDS slots while their words stay in
-//      the window (assign_slots, PendingRows) and reach the matrix once.
+//      of cold input rows collect in a few LDS slots while their words stay
+//      in the window (assign_slots, PendingRows) and reach the matrix once.
 // It serves every compiled shape, including output blocks that take several
 // reductions. The export variant stops after step 2 and writes the
 // minibatches out.
@@ -91,11 +92,11 @@ __global__ __launch_bounds__(kWave) void k_epoch(EpochArgs a) {
   __shared__ SentenceLds sl;
   __shared__ TargetBatch tb;
   __shared__ MinibatchLds mb;
-  extern __shared__ int32_t negs_lds[];  // [kWave][K], then the row slots
+  extern __shared__ int32_t negs_lds[];  // [TB][K], then the pending slots
   const int lane = threadIdx.x;
   const int K = a.K;
   const bool want_loss = a.loss != nullptr;
-  const int TB = kExport ? kWave : a.target_batch;
+  const int TB = kExport ? kWave : a.target_batch;  // targets formed at once
   float* const slot_rows = reinterpret_cast<float*>(negs_lds + TB * (K > 0 ? K : 1));
   const int nslots = kExport ? 0 : a.pend_slots;
   int slot_id = -1, slot_t = 0;
