@@ -326,7 +326,7 @@ size_t w2v_step_batch_sorted_workspace_bytes(int32_t B, int32_t N, int32_t K,
  * are written to staging rows, sorted by row id with a stable radix sort
  * (so a row's updates stay in minibatch order) and summed per row in fp64
  * in that order, in chunks of 64 whose partial sums are added in chunk
- * order. The result is the same bits on every run, and no atomics are
+ * order (grouped 32 chunks at a time). The result is the same bits on every run, and no atomics are
  * used. It may differ from w2v_step_batch, whose fp64 atomics add in
  * arrival order, in the last fp32 bit of an element.
  * Additional limit: B (N + K + 1) must fit in int32. workspace: device,

@@ -15,10 +15,12 @@
 //      inside the chunk is applied (M = fp32(M + sum) where the sum is not
 //      0); the part of a run that crosses the chunk's first or last border
 //      goes to the chunk's head or tail piece;
-//   4. k_reduce_cross: the chunk in which a crossing run starts finds the
-//      run's last chunk (galloping search over chunk borders), adds the head
-//      pieces of the chunks it runs through in chunk order, and applies the
-//      total.
+//   4. k_reduce_spans: a run's head pieces within one span of kSpan chunks
+//      are added, in chunk order, into the first of them;
+//   5. k_reduce_cross: the chunk in which a crossing run starts finds the
+//      run's last chunk (galloping search over chunk borders), adds its
+//      tail piece and the run's summed piece of every span it goes through,
+//      in span order, and applies the total.
 // Traffic per batch: the gathered rows, one staging row written and read
 // per update, the keys, and one read and write per touched row.
 #include <hip/hip_runtime.h>
@@ -229,6 +231,72 @@ __global__ __launch_bounds__(kWave) void k_reduce(ReduceArgs r) {
   }
 }
 
+// Chunks per span: the head pieces of one run inside one span of kSpan
+// chunks are first added into the span's first such piece, so that a run
+// over many chunks costs its start chunk one read per span.
+constexpr int kSpan = 32;
+
+// Key of the first entry of chunk c, and whether its run began earlier.
+__device__ __forceinline__ bool has_head(const ReduceArgs& r, int64_t c,
+                                         uint32_t& key) {
+  const int64_t lo = c * kChunk;
+  if (lo <= 0 || lo >= r.n) return false;
+  key = r.key[lo];
+  return key < 2u * (uint32_t)r.V && r.key[lo - 1] == key;
+}
+
+// Adds `count` piece rows at pieces[2 (c0 + i)] (i < count), a batch at a
+// time, in order.
+template <int C>
+__device__ __forceinline__ void add_heads(const ReduceArgs& r, int64_t c0,
+                                          int64_t count, int lane,
+                                          double (&sum)[C]) {
+  for (int64_t i0 = 0; i0 < count; i0 += kBatch) {
+    double x[kBatch][C];
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      // past the end: re-read the last piece, not added below
+      const int64_t cu = c0 + (i0 + u < count ? i0 + u : count - 1);
+      const double* head = r.pieces + 2 * cu * r.pstride + lane;
+#pragma unroll
+      for (int c = 0; c < C; ++c) x[u][c] = head[kWave * c];
+    }
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u)
+      if (i0 + u < count)
+#pragma unroll
+        for (int c = 0; c < C; ++c) sum[c] += x[u][c];
+  }
+}
+
+// For every (run, span) with head pieces, the wavefront of the first such
+// chunk adds the run's head pieces in the span, in chunk order, into that
+// chunk's head piece.
+template <int C>
+__global__ __launch_bounds__(kWave) void k_reduce_spans(ReduceArgs r) {
+  const int lane = threadIdx.x;
+  const int64_t n_chunks = (r.n + kChunk - 1) / kChunk;
+  for (int64_t ch = blockIdx.x; ch < n_chunks; ch += gridDim.x) {
+    uint32_t key;
+    if (!has_head(r, ch, key)) continue;
+    uint32_t kp;
+    if (ch % kSpan != 0 && has_head(r, ch - 1, kp) && kp == key) continue;
+    // The run's head pieces in this span: chunks ch, ch+1, ... (lane j
+    // tests chunk ch + 1 + j; the run's chunks are consecutive).
+    const int64_t span_end = (ch / kSpan + 1) * kSpan;
+    const int64_t cj = ch + 1 + lane;
+    uint32_t kj = 0u;
+    const bool same = cj < span_end && has_head(r, cj, kj) && kj == key;
+    const int64_t end = ch + 1 + __builtin_ctzll(~__ballot(same));
+    if (end == ch + 1) continue;  // a single head piece is its own sum
+    double sum[C];
+#pragma unroll
+    for (int c = 0; c < C; ++c) sum[c] = 0.0;
+    add_heads<C>(r, ch, end - ch, lane, sum);
+    put_piece<C>(r, ch, 0, lane, sum);
+  }
+}
+
 template <int C>
 __global__ __launch_bounds__(kWave) void k_reduce_cross(ReduceArgs r) {
   const int lane = threadIdx.x;
@@ -264,21 +332,22 @@ __global__ __launch_bounds__(kWave) void k_reduce_cross(ReduceArgs r) {
     const double* tail = r.pieces + (2 * ch + 1) * r.pstride + lane;
 #pragma unroll
     for (int c = 0; c < C; ++c) sum[c] = tail[kWave * c];
-    // Head pieces of chunks ch+1 .. last_chunk, loaded a batch at a time and
-    // added in chunk order.
-    for (int64_t c0 = ch + 1; c0 <= last_chunk; c0 += kBatch) {
+    // One summed piece per span the run goes through (k_reduce_spans), in
+    // span order: the first at ch + 1, the others at span starts.
+    const int64_t first_span = (ch + 1) / kSpan, last_span = last_chunk / kSpan;
+    for (int64_t sp0 = first_span; sp0 <= last_span; sp0 += kBatch) {
       double x[kBatch][C];
 #pragma unroll
       for (int u = 0; u < kBatch; ++u) {
-        // past the run: re-read its last piece, not added below
-        const int64_t cu = c0 + u <= last_chunk ? c0 + u : last_chunk;
-        const double* head = r.pieces + 2 * cu * r.pstride + lane;
+        const int64_t sp = sp0 + u <= last_span ? sp0 + u : last_span;
+        const int64_t c1 = sp == first_span ? ch + 1 : sp * kSpan;
+        const double* head = r.pieces + 2 * c1 * r.pstride + lane;
 #pragma unroll
         for (int c = 0; c < C; ++c) x[u][c] = head[kWave * c];
       }
 #pragma unroll
       for (int u = 0; u < kBatch; ++u)
-        if (c0 + u <= last_chunk)
+        if (sp0 + u <= last_span)
 #pragma unroll
           for (int c = 0; c < C; ++c) sum[c] += x[u][c];
     }
@@ -302,11 +371,12 @@ static StageKernel stage_kernel_for(int C, int nmax, int K) {
   return nullptr;
 }
 
-static bool reduce_kernels_for(int C, ReduceKernel& red, ReduceKernel& cross) {
+static bool reduce_kernels_for(int C, ReduceKernel& red, ReduceKernel& spans,
+                               ReduceKernel& cross) {
   switch (C) {
 #define W2V_CASE(c) \
   case c:           \
-    red = k_reduce<c>; cross = k_reduce_cross<c>; return true;
+    red = k_reduce<c>; spans = k_reduce_spans<c>; cross = k_reduce_cross<c>; return true;
     W2V_CASE(1) W2V_CASE(2) W2V_CASE(3) W2V_CASE(4) W2V_CASE(5) W2V_CASE(6)
     W2V_CASE(8) W2V_CASE(10)
 #undef W2V_CASE
@@ -368,15 +438,15 @@ size_t sorted_step_workspace_bytes(int32_t B, int32_t N, int32_t K, int32_t V,
 }
 
 bool sorted_step_supported(int C, int nmax) {
-  ReduceKernel r, x;
-  return stage_kernel_for(C, nmax, 0) != nullptr && reduce_kernels_for(C, r, x);
+  ReduceKernel r, sp, x;
+  return stage_kernel_for(C, nmax, 0) != nullptr && reduce_kernels_for(C, r, sp, x);
 }
 
 hipError_t launch_step_sorted(int C, int nmax, SortedStepArgs a, void* workspace,
                               hipStream_t s) {
   StageKernel k = stage_kernel_for(C, nmax, a.K);
-  ReduceKernel red, cross;
-  if (k == nullptr || !reduce_kernels_for(C, red, cross)) return hipErrorInvalidValue;
+  ReduceKernel red, spans, cross;
+  if (k == nullptr || !reduce_kernels_for(C, red, spans, cross)) return hipErrorInvalidValue;
   const SortedLayout L = sorted_layout(a.B, a.N, a.K, a.V, (int32_t)a.ld);
   char* w = (char*)workspace;
   float* stage = (float*)w;
@@ -408,6 +478,7 @@ hipError_t launch_step_sorted(int C, int nmax, SortedStepArgs a, void* workspace
   const int64_t n_chunks = (L.n + kChunk - 1) / kChunk;
   const int rgrid = (int)(n_chunks < 65536 ? n_chunks : 65536);
   hipLaunchKernelGGL(red, dim3(rgrid), dim3(kWave), 0, s, r);
+  hipLaunchKernelGGL(spans, dim3(rgrid), dim3(kWave), 0, s, r);
   hipLaunchKernelGGL(cross, dim3(rgrid), dim3(kWave), 0, s, r);
   return hipGetLastError();
 }
