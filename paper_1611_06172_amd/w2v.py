@@ -339,9 +339,9 @@ def step_batch(targets, contexts, negatives, M_in, M_out, alpha=0.025, *,
         if sorted:
             n = step_batch_sorted_workspace_bytes(B, N, K, V, ld)
             if n == 0:
-                _check(lib().w2v_step_batch_sorted(
-                    B, N, K, None, None, None, None, 0.0, None, None, V, D, ld,
-                    None, 0, None, None))
+                raise W2VError(EINVAL if min(B, N, K) < 0 else EHIP,
+                               "no workspace size for this batch (invalid shape "
+                               "or failed sort size query)")
             workspace = torch.empty(n, dtype=torch.uint8, device=M_in.device)
         else:
             workspace = alloc_workspace(V, ld, M_in.device)
