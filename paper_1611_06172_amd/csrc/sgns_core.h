@@ -35,11 +35,12 @@
 // kSplitParts, i.e. its XCD under round-robin dispatch), and reads return
 // the matrix row plus every partial row, so atomics to one address come from
 // one XCD only and nothing is hidden from a reader. Snapshot batches add
-// their updates with fp64 atomics into a delta buffer instead.
+// their updates with fp64 atomics into a delta buffer instead, or write them
+// to staging rows for a sorted reduction (StagedRows).
 //
 // Pending input-row updates (PendingRows): consecutive targets of a
 // sentence share most of their input words, so a training wavefront adds
-// the updates of an input row to an LDS slot instead of the matrix, reads
+// the updates of a cold input row to an LDS slot instead of the matrix, reads
 // the row as (matrix row + its pending updates) while the word stays in the
 // window, and adds the slot to the matrix once, atomically, when it lets
 // the word go. The row traffic of the minibatch path is dominated by its
@@ -352,8 +353,9 @@ struct StagedRows {
 // distinct output columns in mb.out/mb.wgt. Rows id < split_rows of matrix m
 // (0: input, 1: output) have partial rows part[((m split_rows + id)
 // kSplitParts + g) ld], g < kSplitParts (live matrices only). `err` gives
-// the error of a slot (TargetError for one target); `pend` holds input-row
-// updates not yet added to the matrix (NoPendingRows: none).
+// the error of a slot (TargetError for one target); `pend` may take updates
+// instead of the matrices: pending input rows (PendingRows), staging rows
+// (StagedRows), or none (NoPendingRows).
 // Every lane returns its share of the minibatch loss in `loss_part` when
 // want_loss is set.
 template <int C, int NMAX, bool kMulti, bool kLiveRead, bool kAccum64,
