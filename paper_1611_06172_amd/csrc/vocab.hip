@@ -31,9 +31,9 @@ namespace w2v {
 // goes to the global count directly), then adds every table entry to the
 // global counts and clears the table. Head words take a slot early in
 // every chunk, so they cost one global atomic per chunk and workgroup.
-constexpr int kTableSlots = 4096;
+constexpr int kTableSlots = 16384;  // 128 KB of LDS: one workgroup per CU
 constexpr int kProbes = 8;
-constexpr int kCountThreads = 256;
+constexpr int kCountThreads = 1024;
 constexpr int64_t kChunkTokens = (int64_t)kCountThreads * 1024;
 constexpr int32_t kEmptySlot = -1;
 
@@ -52,7 +52,7 @@ __global__ __launch_bounds__(kCountThreads) void k_vocab_count(
     for (int64_t p = ch * kChunkTokens + threadIdx.x; p < end; p += kCountThreads) {
       const int32_t x = raw[p];
       if (x < 0 || x >= V) continue;
-      const uint32_t h = ((uint32_t)x * 2654435761u) >> 20;  // 12 bits
+      const uint32_t h = ((uint32_t)x * 2654435761u) >> 18;  // 14 bits
       bool done = false;
       for (int probe = 0; probe < kProbes && !done; ++probe) {
         const int sl = (int)((h + (uint32_t)probe) & (kTableSlots - 1));
