@@ -12,7 +12,9 @@ pytestmark = pytest.mark.gpu
 
 
 @pytest.mark.parametrize("V_raw,T,min_count", [
-    (8, 16, 2), (50_000, 1_000_000, 3), (1000, 0, 0), (300, 5000, 10_000), (1, 10, 0)])
+    (8, 16, 2), (50_000, 1_000_000, 3), (1000, 0, 0), (300, 5000, 10_000), (1, 10, 0),
+    (200_000, 5_000_001, 5),   # several 2^20-token chunks; tables overflow
+])
 def test_vocab_matches_reference(V_raw, T, min_count):
     import torch
     if V_raw == 8:
