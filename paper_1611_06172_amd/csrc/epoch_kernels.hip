@@ -87,8 +87,21 @@ __device__ __forceinline__ void assign_slots(MinibatchLds& mb, int n, int qj,
   __syncthreads();
 }
 
+// Waves per SIMD the register allocation must allow, where the default
+// allocation lands just above a residency step: at C <= 2 with several
+// output blocks (178 registers, 2 waves) a bound of 3 costs three spilled
+// registers; at C = 10 with one block (256 + 20 registers, 1 wave) a bound of
+// 2 costs 26. Both measured faster (D = 100, K = 15: +9%; D = 600, K = 5:
+// +19%). Both bounds apply to the kernels of up to 10 input words (window
+// <= 5); elsewhere, and at wider windows, the next step up spills too much.
+template <int C, int NMAX, bool kMulti>
+constexpr int epoch_waves_per_eu() {
+  return NMAX > 10 ? 1 : (C <= 2 && kMulti) ? 3 : ((C >= 10 && !kMulti) ? 2 : 1);
+}
+
 template <int C, int NMAX, bool kMulti, bool kExport>
-__global__ __launch_bounds__(kWave) void k_epoch(EpochArgs a) {
+__global__ __launch_bounds__(kWave) __attribute__((
+    amdgpu_waves_per_eu(epoch_waves_per_eu<C, NMAX, kMulti>()))) void k_epoch(EpochArgs a) {
   __shared__ SentenceLds sl;
   __shared__ TargetBatch tb;
   __shared__ MinibatchLds mb;

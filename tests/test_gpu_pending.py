@@ -54,6 +54,8 @@ CASES = [
     (3000, 300, 5, 25, 1e-3, 1000, 0, 0),    # several output blocks
     (1000, 300, 5, 5, 0.0, 1000, 40, 0),     # atomic head rows
     (1000, 64, 5, 5, 0.0, 1000, 37, 3),      # split head rows
+    (800, 600, 5, 5, 1e-3, 1000, 30, 0),     # 10 columns per lane
+    (700, 100, 5, 15, 0.0, 1000, 0, 2),      # 2 columns, several output blocks
 ]
 
 

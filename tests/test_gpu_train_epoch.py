@@ -101,6 +101,10 @@ def test_serialised_plain_mixed_and_split_update_paths(hot, split):
     (300, 200, 8, 3, 0.0, 1000),    # window 8: 16 inputs, blocks of 4
     (200, 72, 16, 1, 1e-2, 1024),   # window 16: 32 inputs, blocks of 2
     (500, 300, 5, 0, 0.0, 50),      # no negatives, short sentences
+    (800, 600, 5, 5, 1e-3, 1000),   # 10 columns per lane (registers bounded
+                                    # for two waves per SIMD)
+    (700, 100, 5, 15, 0.0, 1000),   # 2 columns, several output blocks
+                                    # (bounded for three waves per SIMD)
 ])
 def test_serialised_shapes(V, D, window, K, sub, L):
     """Serialised epochs against the oracle across input capacities, window
