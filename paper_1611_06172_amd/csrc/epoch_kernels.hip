@@ -88,15 +88,19 @@ __device__ __forceinline__ void assign_slots(MinibatchLds& mb, int n, int qj,
 }
 
 // Waves per SIMD the register allocation must allow, where the default
-// allocation lands just above a residency step: at C <= 2 with several
-// output blocks (178 registers, 2 waves) a bound of 3 costs three spilled
-// registers; at C = 10 with one block (256 + 20 registers, 1 wave) a bound of
-// 2 costs 26. Both measured faster (D = 100, K = 15: +9%; D = 600, K = 5:
-// +19%). Both bounds apply to the kernels of up to 10 input words (window
-// <= 5); elsewhere, and at wider windows, the next step up spills too much.
+// allocation lands just above a residency step. With several output blocks
+// at C <= 2 (178 registers, 2 waves) a bound of 3 spills three registers;
+// with one block at C = 4 (175, 2 waves) a bound of 3 spills two, and at
+// C = 10 (256 + 20, 1 wave) a bound of 2 spills 26. Each measured faster
+// (D = 100, K = 15: +9%; D = 200, K = 5: +5%; D = 600, K = 5: +19%). The
+// bounds apply to the kernels of up to 10 input words (window <= 5);
+// elsewhere, and at C = 5 (3 waves: 29 spills, no LDS left for pending
+// rows, -8%), the next step up costs more than it gains.
 template <int C, int NMAX, bool kMulti>
 constexpr int epoch_waves_per_eu() {
-  return NMAX > 10 ? 1 : (C <= 2 && kMulti) ? 3 : ((C >= 10 && !kMulti) ? 2 : 1);
+  if (NMAX > 10) return 1;
+  if (kMulti) return C <= 2 ? 3 : 1;
+  return C == 4 ? 3 : (C >= 10 ? 2 : 1);
 }
 
 template <int C, int NMAX, bool kMulti, bool kExport>

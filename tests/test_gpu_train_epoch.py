@@ -105,6 +105,8 @@ def test_serialised_plain_mixed_and_split_update_paths(hot, split):
                                     # for two waves per SIMD)
     (700, 100, 5, 15, 0.0, 1000),   # 2 columns, several output blocks
                                     # (bounded for three waves per SIMD)
+    (900, 200, 5, 5, 1e-3, 1000),   # 4 columns, one output block (bounded
+                                    # for three waves per SIMD)
 ])
 def test_serialised_shapes(V, D, window, K, sub, L):
     """Serialised epochs against the oracle across input capacities, window
