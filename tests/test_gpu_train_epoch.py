@@ -224,6 +224,34 @@ def test_hogwild_epochs_near_sequential(update_path, inflight, bound, algorithm)
     assert abs(lg - lo) <= bound * lo, (lg, lo, l0)
 
 
+@pytest.mark.parametrize("D,K", [(600, 5), (200, 5), (100, 15)])
+def test_hogwild_register_bounded_shapes(D, K):
+    """Concurrent epochs of the kernels compiled with a register bound (and
+    so with spilled registers): 64 sentences in flight over 20,000 words
+    with the conflict model's atomic rows; the training-loss trajectory of
+    two epochs within 2% of the sequential oracle's."""
+    import torch
+    V, E = 20_000, 2
+    corpus, table, M_in, M_out = tiny_config(T=200_000, V=V, D=D)
+    kw = dict(window=5, K=K, sentence_len=1000, seed=13, alpha0=0.025, n_epochs=E)
+    hot = w2v.hot_rows(inputs.word_counts(corpus, V), sample_t=0.0, K=K, inflight=64)
+    o_in, o_out = M_in.copy(), M_out.copy()
+    gi, go = to_dev(M_in), to_dev(M_out)
+    c, tb = to_dev(corpus), to_dev(table)
+    print(f"[hogwild-bounded] D={D} K={K} hot={hot}", flush=True)
+    for e in range(E):
+        n, ob = oracle.train_epoch(oracle.Sampling(corpus, table, None, epoch=e, **kw),
+                                   o_in, o_out, n_buckets=1)
+        lb = torch.zeros((1, 2), dtype=torch.float64, device="cuda")
+        w2v.train_epoch(c, gi, go, tb, None, epoch=e, loss_buckets=lb, hot_rows=hot,
+                        max_inflight=64, **kw)
+        gb = lb.cpu().numpy()
+        assert gb[0, 1] == ob[0, 1]
+        lo, lg = ob[0, 0] / ob[0, 1], gb[0, 0] / gb[0, 1]
+        assert abs(lg - lo) <= 0.02 * lo, (e, lg, lo)
+    assert np.isfinite(gi.cpu().numpy()).all() and np.isfinite(go.cpu().numpy()).all()
+
+
 def test_sentence_aligned_chunks_equal_one_call_when_serialised():
     corpus, table, M_in, M_out = tiny_config(T=30_000)
     kw = dict(window=5, K=5, sentence_len=1000, seed=2, max_inflight=1)
