@@ -336,12 +336,41 @@ int32_t oracle_pair_negative(const oracle_sampling* s, int64_t p, int32_t i,
   return s->neg_table[((uint64_t)r * (uint64_t)s->table_size) >> 32];
 }
 
-/* One target: returns -1 when an id is out of range (nothing is applied),
- * else 0; adds the pairs' losses to *loss. */
+/* One SGD step of the logistic loss of a single (input vector, output row)
+ * pair, the unit Alg. 1 works in. With x = v . u and label l (1 for the
+ * target, 0 for a negative), the pair's loss is -log sigma(x) or
+ * -log sigma(-x); its gradient is -(l - sigma(x)) v with respect to u and
+ * -(l - sigma(x)) u with respect to v. The output row takes its step at once
+ * (rounded to fp32 as it is stored); the step of the input vector is added
+ * into v_step, because the input vector stays fixed until all of its word's
+ * pairs have run. u is scratch. Returns the pair's loss. */
+static double logistic_pair_step(const double* v, float* out_row, int32_t D,
+                                 double label, double alpha, double* u,
+                                 double* v_step) {
+  double x = 0.0;
+  for (int32_t j = 0; j < D; ++j) {
+    u[j] = (double)out_row[j];
+    x += v[j] * u[j];
+  }
+  const double coef = alpha * (label - sigma(x));
+  for (int32_t j = 0; j < D; ++j) {
+    v_step[j] += coef * u[j];
+    out_row[j] = (float)(u[j] + coef * v[j]);
+  }
+  return -log_sigma(label > 0.0 ? x : -x);
+}
+
+/* The Alg. 1 update of one target word: returns -1 when an id is out of
+ * range (nothing is applied), else 0, and adds the pairs' losses to *loss.
+ * Input words are taken in window order. Each one pairs with the target
+ * (label 1) and then with its own K draws (label 0; a draw equal to the
+ * target forms no pair), every pair stepping the output row as the pairs
+ * before it left it; the input word's row then moves by the sum of its
+ * pairs' steps. v, u and v_step are D doubles of scratch. */
 static int alg1_target(const oracle_sampling* s, float* M_in, float* M_out,
                        int32_t V, int32_t D, int32_t ld, int64_t p,
                        int32_t target, const int32_t* ctx, int32_t n,
-                       float alpha, double* a, double* o, double* temp,
+                       float alpha, double* v, double* u, double* v_step,
                        double* loss) {
   if (target < 0 || target >= V) return -1;
   for (int32_t i = 0; i < n; ++i) {
@@ -351,34 +380,20 @@ static int alg1_target(const oracle_sampling* s, float* M_in, float* M_out,
       if (neg < 0 || neg >= V) return -1;
     }
   }
+  const double a = (double)alpha;
   for (int32_t i = 0; i < n; ++i) {
     float* in_row = M_in + (size_t)ctx[i] * ld;
     for (int32_t j = 0; j < D; ++j) {
-      a[j] = (double)in_row[j];
-      temp[j] = 0.0;
+      v[j] = (double)in_row[j];
+      v_step[j] = 0.0;
     }
-    for (int32_t k = 0; k <= s->K; ++k) {
-      int32_t word = target;
-      double label = 1.0;
-      if (k > 0) {
-        word = oracle_pair_negative(s, p, i, k - 1);
-        label = 0.0;
-        if (word == target) continue;
-      }
-      float* out_row = M_out + (size_t)word * ld;
-      double inner = 0.0;
-      for (int32_t j = 0; j < D; ++j) {
-        o[j] = (double)out_row[j];
-        inner += a[j] * o[j];
-      }
-      double err = (double)alpha * (label - sigma(inner));
-      *loss -= log_sigma(label > 0.0 ? inner : -inner);
-      for (int32_t j = 0; j < D; ++j) {
-        temp[j] += err * o[j];
-        out_row[j] = (float)(o[j] + err * a[j]);
-      }
+    *loss += logistic_pair_step(v, M_out + (size_t)target * ld, D, 1.0, a, u, v_step);
+    for (int32_t k = 0; k < s->K; ++k) {
+      const int32_t drawn = oracle_pair_negative(s, p, i, k);
+      if (drawn == target) continue;
+      *loss += logistic_pair_step(v, M_out + (size_t)drawn * ld, D, 0.0, a, u, v_step);
     }
-    for (int32_t j = 0; j < D; ++j) in_row[j] = (float)(a[j] + temp[j]);
+    for (int32_t j = 0; j < D; ++j) in_row[j] = (float)(v[j] + v_step[j]);
   }
   return 0;
 }
@@ -393,12 +408,12 @@ int64_t oracle_pairwise_train_epoch(const oracle_sampling* s, float* M_in,
   oracle_sentence sen;
   if (oracle_sentence_alloc(&sen, s->sentence_len, s->window, s->K) != 0)
     return -2;
-  double* a = (double*)malloc(sizeof(double) * (size_t)D);
-  double* o = (double*)malloc(sizeof(double) * (size_t)D);
-  double* temp = (double*)malloc(sizeof(double) * (size_t)D);
+  double* v = (double*)malloc(sizeof(double) * (size_t)D);
+  double* u = (double*)malloc(sizeof(double) * (size_t)D);
+  double* v_step = (double*)malloc(sizeof(double) * (size_t)D);
   const int32_t w2 = 2 * s->window;
   int64_t applied = 0;
-  int status = (a && o && temp) ? 0 : -2;
+  int status = (v && u && v_step) ? 0 : -2;
   for (int64_t sb = s->pos_begin; sb < s->pos_end && status == 0;
        sb += s->sentence_len) {
     int64_t se = sb + s->sentence_len;
@@ -408,7 +423,7 @@ int64_t oracle_pairwise_train_epoch(const oracle_sampling* s, float* M_in,
       double loss = 0.0;
       status = alg1_target(s, M_in, M_out, V, D, ld, sen.pos[m], sen.target[m],
                            sen.ctx + (size_t)m * w2, sen.n_ctx[m], sen.alpha[m],
-                           a, o, temp, &loss);
+                           v, u, v_step, &loss);
       if (status != 0) break;
       if (loss_buckets != NULL) {
         int64_t b = sen.pos[m] * (int64_t)n_buckets / s->T;
@@ -418,7 +433,7 @@ int64_t oracle_pairwise_train_epoch(const oracle_sampling* s, float* M_in,
       ++applied;
     }
   }
-  free(a); free(o); free(temp);
+  free(v); free(u); free(v_step);
   oracle_sentence_free(&sen);
   return status == 0 ? applied : status;
 }

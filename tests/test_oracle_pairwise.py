@@ -116,3 +116,60 @@ def test_untouched_rows_and_training_lowers_loss():
     assert losses[1] < losses[0] and losses[2] < losses[0]
     assert np.array_equal(a_in[200:].view(np.uint32), M_in[200:].view(np.uint32))
     assert not a_out[200:].any()
+
+
+def test_matches_an_independent_per_pair_restatement():
+    """Alg. 1 restated independently in numpy from the per-pair logistic
+    step (for each input word in window order: the target pair, then that
+    word's own draws, a draw equal to the target forming no pair; each pair
+    reads its output row as the earlier pairs left it and writes it back at
+    once; the input row moves by the sum of its pairs' steps after its last
+    pair), on the minibatches and private draws of the oracle's sampling
+    (pinned elsewhere). A three-word table makes private draws repeat within
+    one input word's K and across input words, and hit the target. The two
+    agree to within one fp32 rounding per write of the row (fp64 inner
+    products summed in another order)."""
+    V, D = 12, 8
+    corpus = np.array([0, 3, 1, 4, 2, 5, 0, 6, 1, 7, 2, 8, 0, 9, 1, 10, 2, 11, 3, 4,
+                       5, 6, 0, 1, 2, 7, 8, 9, 10, 11, 0, 2, 4, 6, 8, 10, 1, 3, 5, 7],
+                      np.int32)
+    table = np.array([0] * 5 + [1] * 3 + [2] * 2, np.int32)
+    M_in = inputs.init_matrix(V, D, "normal", 20, scale=0.4)
+    M_out = inputs.init_matrix(V, D, "normal", 21, scale=0.4)
+    kw = dict(window=3, K=3, sentence_len=len(corpus), seed=22, alpha0=0.1)
+    s = oracle.Sampling(corpus, table, None, **kw)
+    mb = oracle.minibatches(s)
+
+    r_in, r_out = M_in.astype(np.float32).copy(), M_out.astype(np.float32).copy()
+    writes_in, writes_out = np.zeros(V, int), np.zeros(V, int)
+    saw_repeat = saw_hit = saw_three = False
+    for m in range(len(mb["targets"])):
+        t, a = int(mb["targets"][m]), float(mb["alpha"][m])
+        inputs_m = [int(c) for c in mb["ctx"][m] if c >= 0]
+        draws = oracle.pair_negatives(s, int(mb["pos"][m]), len(inputs_m))
+        saw_three |= len(inputs_m) >= 3
+        for i, c in enumerate(inputs_m):
+            saw_repeat |= len(set(draws[i].tolist())) < kw["K"]
+            saw_hit |= bool((draws[i] == t).any())
+            pairs = [(t, 1.0)] + [(int(w), 0.0) for w in draws[i] if w != t]
+            v = r_in[c].astype(np.float64)
+            step = np.zeros(D)
+            for w, label in pairs:
+                u = r_out[w].astype(np.float64)
+                g = a * (label - 1.0 / (1.0 + np.exp(-float(np.dot(v, u)))))
+                step += g * u
+                r_out[w] = (u + g * v).astype(np.float32)
+                writes_out[w] += 1
+            r_in[c] = (v + step).astype(np.float32)
+            writes_in[c] += 1
+    assert saw_repeat and saw_hit and saw_three
+
+    o_in, o_out = M_in.copy(), M_out.copy()
+    n, _ = oracle.pairwise_train_epoch(s, o_in, o_out)
+    assert n == len(mb["targets"])
+    for got, ref, writes in ((o_in, r_in, writes_in), (o_out, r_out, writes_out)):
+        ulp = np.spacing(np.maximum(np.abs(got), np.abs(ref)).astype(np.float32))
+        bound = np.maximum(writes, 1)[:, None] * ulp
+        assert np.all(np.abs(got.astype(np.float64) - ref) <= bound), \
+            np.max(np.abs(got.astype(np.float64) - ref) / ulp)
+    assert writes_in.sum() >= 3 and writes_out.max() >= 3

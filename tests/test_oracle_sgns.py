@@ -318,3 +318,90 @@ def test_epoch_training_lowers_loss():
         per_ctx.append(b[0, 0] / b[0, 1])
     assert per_ctx[0] < 6 * math.log(2)
     assert per_ctx[2] < per_ctx[0] * 0.95
+
+
+def test_error_scales_of_a_hand_worked_minibatch():
+    """The tolerance scales of the snapshot batch on a case worked by hand.
+    N = 2, K = 1, D = 2; every input row is parallel to (1, 1) and every
+    output row to (1, -1), so all logits are 0, sigma = 1/2 and with
+    alpha = 1/2 the errors are E_i0 = +1/4 (target) and E_i1 = -1/4
+    (negative). A_0 = (1, 1), A_1 = (-1/2, -1/2), O_0 = (1/4, -1/4),
+    O_1 = (1/2, -1/2), all dyadic, so every value below is exact:
+      dA_i = 1/4 O_0 - 1/4 O_1 = (-1/16, 1/16)
+      sA_i = 1/4 |O_0| + 1/4 |O_1| = (3/16, 3/16)
+      dO_0 = 1/4 (A_0 + A_1) = (1/8, 1/8),  sO_0 = 1/4 (|A_0| + |A_1|) = (3/8, 3/8)
+      dO_1 = -dO_0,                         sO_1 = sO_0
+      loss = 4 ln 2.
+    The batch holds this minibatch twice, so S = |M0| + 2 s per element and
+    the update is doubled; rows no minibatch touches have S = |M0|."""
+    A = np.array([[1.0, 1.0], [-0.5, -0.5]])
+    O = np.array([[0.25, -0.25], [0.5, -0.5]])
+    X, dA, dO, loss, sA, sO = oracle.sgns_delta_scaled(A, O, np.zeros(1, np.uint8), 0.5)
+    assert np.array_equal(X, np.zeros((2, 2)))
+    assert np.array_equal(dA, np.full((2, 2), 1 / 16) * [-1, 1])
+    assert np.array_equal(sA, np.full((2, 2), 3 / 16))
+    assert np.array_equal(dO, np.array([[1 / 8, 1 / 8], [-1 / 8, -1 / 8]]))
+    assert np.array_equal(sO, np.full((2, 2), 3 / 8))
+    assert loss == pytest.approx(4 * np.log(2), rel=1e-15)
+
+    V = 6   # rows: inputs 1, 2; target 3; negative 4; 0 and 5 untouched
+    M_in = np.full((V, 2), 0.125, np.float32) * [1, -1]
+    M_in[1], M_in[2] = A[0], A[1]
+    M_out = np.full((V, 2), -0.375, np.float32)
+    M_out[3], M_out[4] = O[0], O[1]
+    t = np.array([3, 3], np.int32)
+    c = np.array([[1, 2], [1, 2]], np.int32)
+    n = np.array([[4], [4]], np.int32)
+    Mi, Mo, S_in, S_out = oracle.step_batch(t, c, n, M_in, M_out, 0.5)
+    exp_S_in = np.abs(M_in).astype(np.float64)
+    exp_S_in[[1, 2]] += 2 * 3 / 16
+    exp_S_out = np.abs(M_out).astype(np.float64)
+    exp_S_out[[3, 4]] += 2 * 3 / 8
+    assert np.array_equal(S_in, exp_S_in)
+    assert np.array_equal(S_out, exp_S_out)
+    exp_in = M_in.astype(np.float64)
+    exp_in[[1, 2]] += 2 * np.array([-1 / 16, 1 / 16])
+    exp_out = M_out.astype(np.float64)
+    exp_out[3] += 2 * np.array([1 / 8, 1 / 8])
+    exp_out[4] -= 2 * np.array([1 / 8, 1 / 8])
+    assert np.array_equal(Mi, exp_in.astype(np.float32))
+    assert np.array_equal(Mo, exp_out.astype(np.float32))
+
+
+def test_error_scales_bounded_above():
+    """Upper bound of the scales that does not use the oracle's arithmetic:
+    |alpha (l - sigma)| <= alpha, so an input row's S exceeds |M0| by at most
+    alpha sum over its occurrences of sum_k |O_k| (the column's output rows,
+    masked columns included) and an output row's by at most alpha sum over its
+    occurrences of sum_i |A_i|. With alpha small against |M0| this catches
+    a scale that counts |M0| twice or adds a term per column more than once;
+    the lower bounds S >= |M0| and S >= |dM| are checked with it."""
+    V, D, B, N, K = 50, 12, 300, 6, 4
+    alpha = 1e-5
+    M_in = inputs.init_matrix(V, D, "normal", 30)
+    M_out = inputs.init_matrix(V, D, "normal", 31)
+    t, c, n = inputs.kernel_batch(B, N, K, V, 1.0, 32)
+    c[5, 2:] = -1
+    n[7, 1] = t[7]                       # a masked column
+    Mi, Mo, S_in, S_out = oracle.step_batch(t, c, n, M_in, M_out, alpha)
+    A0, O0 = np.abs(M_in.astype(np.float64)), np.abs(M_out.astype(np.float64))
+    hi_in, hi_out = A0.copy(), O0.copy()
+    for b in range(B):
+        ins = [int(x) for x in c[b] if x >= 0]
+        outs = [int(t[b])] + [int(x) for x in n[b]]
+        o_sum = O0[outs].sum(axis=0)
+        a_sum = A0[ins].sum(axis=0)
+        for r in ins:
+            hi_in[r] += alpha * o_sum
+        for r in outs:
+            hi_out[r] += alpha * a_sum
+    slack = 1e-12
+    assert np.all(S_in <= hi_in * (1 + slack)) and np.all(S_out <= hi_out * (1 + slack))
+    assert np.all(S_in >= A0) and np.all(S_out >= O0)
+    assert np.all(S_in + 1e-12 >= np.abs(Mi.astype(np.float64) - M_in))
+    assert np.all(S_out + 1e-12 >= np.abs(Mo.astype(np.float64) - M_out))
+    # the bound is tight enough to see |M0| counted twice wherever |M0| is
+    # not small
+    big_in, big_out = A0 > 0.02, O0 > 0.02
+    assert np.all(hi_in[big_in] < 1.5 * A0[big_in])
+    assert np.all(hi_out[big_out] < 1.5 * O0[big_out])
