@@ -46,9 +46,10 @@ def kernel_hash():
     return h.hexdigest()[:16]
 
 
-def measured_traffic(path, n_launch_bytes_scale):
-    """HBM bytes per launch from a committed counter summary, if it was taken
-    on the current kernel sources (else None)."""
+def measured_traffic(path):
+    """Counter figures per launch from a committed summary (HBM bytes from the
+    per-request-size memory-side counters, L2 bytes), if it was taken on the
+    current kernel sources (else None)."""
     try:
         with open(path) as f:
             d = json.load(f)
@@ -56,7 +57,31 @@ def measured_traffic(path, n_launch_bytes_scale):
         return None
     if d.get("kernel_hash") != kernel_hash():
         return None
-    return d.get("hbm_bytes_per_launch")
+    return d
+
+
+def on_one_core(fn):
+    """Runs fn() with this process pinned to the first CPU it may use (its
+    GPU work is done by then); returns (result, seconds, cpu, n_cpus)."""
+    allowed = sorted(os.sched_getaffinity(0))
+    os.sched_setaffinity(0, {allowed[0]})
+    try:
+        c0 = time.perf_counter()
+        out = fn()
+        return out, time.perf_counter() - c0, allowed[0], len(allowed)
+    finally:
+        os.sched_setaffinity(0, set(allowed))
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 def main():
@@ -96,7 +121,13 @@ def main():
                          "spread atomics beyond the first one or two words")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="run a 1 GiB device copy first (counter calibration)")
-    ap.add_argument("--cpu-sample-tokens", type=int, default=2_000_000)
+    ap.add_argument("--cpu-sample-tokens", type=int, default=3_000_000,
+                    help="oracle baseline sample: the first tokens of the corpus "
+                         "(about 27 s of one core at 3e6)")
+    ap.add_argument("--literal-steps", type=int, default=3,
+                    help="timed epochs of the paper-literal write-back "
+                         "(hogbatch_immediate) run after the headline, reported "
+                         "beside it (0: skip)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--workload", choices=["large-vocab", "kernel-test", "vocab"],
                     default="large-vocab",
@@ -134,7 +165,7 @@ def main():
     L = 1000
 
     t0 = time.time()
-    corpus = inputs.zipf_corpus_device(T, V, 1.07, 6, dev)
+    corpus = inputs.zipf_corpus_hashed(T, V, 1.07, 6, dev)
     counts = torch.bincount(corpus, minlength=V).cpu().numpy().astype(np.int64)
     table_h, thr_h = w2v.build_tables(counts, 0.75, args.sample, 10**8)
     table = torch.from_numpy(table_h).to(dev)
@@ -143,8 +174,8 @@ def main():
     # rows padded to whole 128-byte lines (ld = 320 floats at D = 300)
     M_in = w2v.alloc_matrix(V, D, dev, torch.from_numpy(M_in0))
     M_out = w2v.alloc_matrix(V, D, dev)
-    stats = torch.zeros(4, dtype=torch.int64, device=dev)
-    inflight = args.max_inflight or w2v.default_inflight(D, W, K)
+    stats = torch.zeros(5, dtype=torch.int64, device=dev)
+    inflight = args.max_inflight or w2v.default_inflight(D, W, K, V=V, group=args.group)
     hot = (args.hot_rows if args.hot_rows >= 0 else
            w2v.hot_rows(counts, sample_t=args.sample, window=W, K=K,
                         inflight=inflight, tol=args.hot_tol))
@@ -169,15 +200,17 @@ def main():
     print(f"[bench] setup {time.time() - t0:.1f}s: T={T} V={V} D={D} K={K} w={W}",
           file=sys.stderr, flush=True)
 
-    n_epochs = args.warmup + args.steps
+    literal = (args.literal_steps if args.algorithm == "hogbatch" and args.group == 1
+               else 0)
+    n_epochs = args.warmup + args.steps + (1 + literal if literal else 0)
 
-    def step(i):
+    def step(i, algorithm=args.algorithm):
         w2v.train_epoch(corpus, M_in, M_out, table, thr, window=W, K=K,
                         alpha0=0.025, min_alpha_frac=1e-4, epoch=i,
                         n_epochs=n_epochs, seed=1234, sentence_len=L,
                         stats=stats, max_inflight=args.max_inflight,
                         hot_rows=hot, split_rows=split, workspace=workspace,
-                        algorithm=args.algorithm, group=args.group)
+                        algorithm=algorithm, group=args.group)
 
     for i in range(args.warmup):
         step(i)
@@ -207,19 +240,21 @@ def main():
     # back its N + K + 1 rows (8 D bytes per row) and reads K table entries;
     # Algorithm 1 moves, per input word, its own row and K + 1 output rows and
     # reads K table entries; every raw word reads its id and keep threshold.
-    n_mb, sum_n, raw = st[0], st[1], st[2]
+    n_mb, sum_n, raw, rows = st[0], st[1], st[2], st[4]
     if args.algorithm == "pairwise":
         alg_bytes = 8.0 * D * sum_n * (K + 2) + 4.0 * K * sum_n + 8.0 * raw
+    elif args.group > 1:
+        # A group reads and writes each of its distinct rows once (stats[4]);
+        # every retained target still draws its K table entries.
+        alg_bytes = 8.0 * D * rows + 4.0 * K * n_mb + 8.0 * raw
     else:
         alg_bytes = 8.0 * D * (sum_n + n_mb * (K + 1)) + 4.0 * K * n_mb + 8.0 * raw
     avg_kern_s = float(np.mean(kern_ms)) / 1e3
     achieved = alg_bytes / avg_kern_s / 1e9
-    traffic = (measured_traffic(args.traffic_json, 1.0)
-               if args.algorithm == "hogbatch" and args.group == 1 else None)
-    # Grouped negatives move one set of output rows per group and each
-    # distinct input row once per group; the kernel keeps no count of those,
-    # so the per-target byte count above would overstate the work.
-    grouped = args.group > 1
+    counters = (measured_traffic(args.traffic_json)
+                if args.algorithm == "hogbatch" and args.group == 1
+                and T == 10**9 and (V, D, K, W) == (10**6, 300, 5, 5) else None)
+    traffic = counters["hbm_bytes_per_launch"] if counters else None
 
     result = {
         "metric": METRIC,
@@ -251,31 +286,76 @@ def main():
             "bound": "hbm",
             "kernel": ("k_epoch_pairwise" if args.algorithm == "pairwise" else
                        "k_epoch_grouped" if args.group > 1 else "k_epoch"),
-            "achieved": None if grouped else round(achieved, 1),
+            "achieved": round(achieved, 1),
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
-            "frac": None if grouped else round(achieved / HBM_PEAK_GBS, 4),
+            "frac": round(achieved / HBM_PEAK_GBS, 4),
             "traffic": traffic,
-            "alg_bytes_per_launch": None if grouped else alg_bytes,
+            "alg_bytes_per_launch": alg_bytes,
+            "achieved_is": "algorithmic bytes (every row of every minibatch read "
+                           "and written once) / launch time",
             "kernel_ms": round(avg_kern_s * 1e3, 3),
         },
     }
-    if grouped:
-        result["roofline"]["note"] = ("grouped negatives: no per-group count of the "
-                                      "rows moved is kept, so no algorithmic bytes")
+    if counters:
+        # Measured at the memory side and in L2 (committed counter run on the
+        # same kernel sources), divided by this run's launch time.
+        hbm_gbs = traffic / avg_kern_s / 1e9
+        result["roofline"]["hbm_measured_GBs"] = round(hbm_gbs, 1)
+        result["roofline"]["hbm_measured_frac"] = round(hbm_gbs / HBM_PEAK_GBS, 4)
+        if counters.get("l2_bytes_per_launch"):
+            result["roofline"]["l2_GBs"] = round(
+                counters["l2_bytes_per_launch"] / avg_kern_s / 1e9, 1)
+        result["roofline"]["counters"] = os.path.relpath(args.traffic_json, ROOT)
+
+    if literal:
+        # The paper's write-back (Sec. 1.1: every update reaches the matrices
+        # at the end of its minibatch) on the same kernel, continuing the
+        # schedule: one untimed epoch, then `literal` timed ones.
+        e0 = args.warmup + args.steps
+        step(e0, "hogbatch_immediate")
+        torch.cuda.synchronize()
+        lev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(literal)]
+        stats.zero_()
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        for i in range(literal):
+            lev[i][0].record(stream)
+            step(e0 + 1 + i, "hogbatch_immediate")
+            lev[i][1].record(stream)
+        torch.cuda.synchronize()
+        lwall = time.perf_counter() - t1
+        lms = float(np.mean([a.elapsed_time(b) for a, b in lev]))
+        lst = stats.cpu().numpy().astype(np.float64) / literal
+        lbytes = 8.0 * D * (lst[1] + lst[0] * (K + 1)) + 4.0 * K * lst[0] + 8.0 * lst[2]
+        result["paper_literal_writeback"] = {
+            "algorithm": "hogbatch_immediate",
+            "value": round(T / (lwall / literal) / 1e6, 3), "unit": "Mwords/s",
+            "steps": literal, "ms_per_step": round(lwall * 1e3 / literal, 3),
+            "roofline_frac": round(lbytes / (lms / 1e3) / 1e9 / HBM_PEAK_GBS, 4),
+            "note": "every input-row update written back at the end of its "
+                    "minibatch (no pending LDS slots); epochs continue the "
+                    "headline run's schedule",
+        }
+        print(f"[bench] paper-literal write-back: {literal} epochs, "
+              f"{lms:.1f} ms per launch", file=sys.stderr, flush=True)
 
     if not args.no_cpu_baseline:
         import oracle
-        n_s = args.cpu_sample_tokens
+        n_s = min(args.cpu_sample_tokens, T)
         sample_corpus = corpus[:n_s].cpu().numpy()
         o_in = M_in0.copy()
         o_out = np.zeros((V, D), dtype=np.float32)
         s = oracle.Sampling(sample_corpus, table_h, thr_h, window=W, K=K,
-                            sentence_len=L, seed=1234)
-        c0 = time.perf_counter()
-        run = oracle.pairwise_train_epoch if args.algorithm == "pairwise" else oracle.train_epoch
-        n_o, _ = run(s, o_in, o_out)
-        c_dt = time.perf_counter() - c0
+                            sentence_len=L, seed=1234, n_epochs=1)
+        if args.algorithm == "pairwise":
+            run = lambda: oracle.pairwise_train_epoch(s, o_in, o_out)  # noqa: E731
+        elif args.group > 1:
+            run = lambda: oracle.grouped_train_epoch(s, args.group, o_in, o_out)  # noqa: E731
+        else:
+            run = lambda: oracle.train_epoch(s, o_in, o_out)  # noqa: E731
+        (n_o, _), c_dt, cpu, n_cpu = on_one_core(run)
         result["cpu_baseline"] = {
             "value": round(n_s / c_dt / 1e6, 5),
             "unit": "Mwords/s",
@@ -283,8 +363,9 @@ def main():
             "kind": "oracle",
             "sample": (f"first {n_s} tokens of the same corpus as a 1-epoch run "
                        f"({n_o} minibatches, same tables and initial M_in), "
-                       f"single-threaded fp64 oracle, {c_dt:.1f}s; host has "
-                       f"{os.cpu_count()} logical CPUs"),
+                       f"single-threaded fp64 oracle pinned to CPU {cpu}, "
+                       f"{c_dt:.1f}s; CPU {cpu_model()}, {n_cpu} CPUs "
+                       f"available to the process"),
         }
     print(json.dumps(result), flush=True)
 
@@ -309,6 +390,11 @@ def kernel_test(args):
     M_out = w2v.alloc_matrix(V, D, dev, torch.from_numpy(Mo0))
     T, C, Ng = (torch.from_numpy(x).to(dev) for x in (t, c, n))
     srt = args.step_mode == "sorted"
+    if args.calibrate_copy:
+        src = torch.empty(1 << 28, dtype=torch.float32, device=dev)
+        src.fill_(1.0)
+        dst = src.clone()
+        del src, dst
     ws = w2v.step_batch(T, C, Ng, M_in, M_out, 0.025, D=D, sorted=srt)  # allocates
     for _ in range(max(args.warmup, 0)):
         w2v.step_batch(T, C, Ng, M_in, M_out, 0.025, D=D, workspace=ws, sorted=srt)
@@ -355,15 +441,14 @@ def kernel_test(args):
     if not args.no_cpu_baseline:
         import oracle
         bs = B
-        c0 = time.perf_counter()
-        oracle.step_batch(t[:bs], c[:bs], n[:bs], Mi0, Mo0, 0.025, D=D, with_scale=False)
-        c_dt = time.perf_counter() - c0
+        _, c_dt, cpu, n_cpu = on_one_core(lambda: oracle.step_batch(
+            t[:bs], c[:bs], n[:bs], Mi0, Mo0, 0.025, D=D, with_scale=False))
         result["cpu_baseline"] = {
             "value": round(bs / c_dt / 1e6, 5), "unit": "Mminibatches/s",
             "cores": 1, "kind": "oracle",
             "sample": (f"the whole batch ({bs} minibatches), single-threaded fp64 "
-                       f"oracle snapshot batch, {c_dt:.1f}s; host has "
-                       f"{os.cpu_count()} logical CPUs"),
+                       f"oracle snapshot batch pinned to CPU {cpu}, {c_dt:.1f}s; "
+                       f"CPU {cpu_model()}, {n_cpu} CPUs available to the process"),
         }
     print(json.dumps(result), flush=True)
 
@@ -442,14 +527,14 @@ def vocab_bench(args):
         import oracle
         n_s = min(T, 100_000_000)
         sample = raw[:n_s].cpu().numpy()
-        c0 = time.perf_counter()
-        oracle.build_vocab(sample, V_raw, min_count)
-        c_dt = time.perf_counter() - c0
+        _, c_dt, cpu, n_cpu = on_one_core(lambda: oracle.build_vocab(sample, V_raw,
+                                                                     min_count))
         result["cpu_baseline"] = {
             "value": round(n_s / c_dt / 1e6, 2), "unit": "Mtokens/s", "cores": 1,
             "kind": "oracle",
-            "sample": (f"first {n_s} raw ids, numpy bincount + stable argsort oracle, "
-                       f"{c_dt:.1f}s; host has {os.cpu_count()} logical CPUs"),
+            "sample": (f"first {n_s} raw ids, numpy bincount + stable argsort oracle "
+                       f"pinned to CPU {cpu}, {c_dt:.1f}s; CPU {cpu_model()}, "
+                       f"{n_cpu} CPUs available to the process"),
         }
     print(json.dumps(result), flush=True)
 

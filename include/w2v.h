@@ -24,10 +24,16 @@
  *   - Return value: W2V_OK (0) or a negative W2V_E* code; w2v_last_error()
  *     then describes the failure. Arguments are validated on the host before
  *     any HIP call; a call that fails validation launches nothing.
- *   - Ids read from device memory (corpus, tables, batches) are checked on the
- *     device: a minibatch that would touch a row outside [0, V) is skipped and
- *     counted in the optional stats output; no memory outside the given
- *     buffers is ever accessed.
+ *   - Ids read from device memory (corpus, tables, batches) are always checked
+ *     on the device: a minibatch that would touch a row outside [0, V) is
+ *     skipped (no memory outside the given buffers is ever accessed), counted
+ *     in the optional stats output, and recorded in the device's error word.
+ *     The first GPU call on that device that starts after the skipping kernel
+ *     has finished returns W2V_EDEVICE_FLAG, clears the word and launches
+ *     nothing; w2v_device_status waits for a stream and reports the same.
+ *     In the corpus, -1 marks a word removed from the vocabulary
+ *     (w2v_build_vocab) and is no error: the position is dropped before
+ *     windows form.
  *
  * Readings of points the paper leaves open (sentence cut, window shrink,
  * subsampling rule, negative distribution, learning-rate decay, random
@@ -48,6 +54,8 @@ extern "C" {
 #define W2V_EHIP (-2)        /* the HIP runtime reported an error */
 #define W2V_ENOMEM (-3)      /* a host allocation failed */
 #define W2V_EUNSUPPORTED (-4)/* valid arguments outside the compiled shapes */
+#define W2V_EDEVICE_FLAG (-5)/* an earlier call skipped work for an id outside
+                                [0, V); nothing was launched by this call */
 
 /* Shape limits of the compiled kernels. The HogBatch kernels keep all N
  * input rows of a minibatch in registers, so they compile D <= 640 for up to
@@ -74,6 +82,18 @@ int w2v_version(void);
 /* Message of the last failed call on this thread ("" if none). The pointer
  * stays valid until the next call on the same thread. */
 const char* w2v_last_error(void);
+
+/* Sets up the library's per-device state on the current HIP device: the
+ * device's error word (pinned host memory mapped into the device, 256 bytes,
+ * held until the process ends). Every GPU entry point does this itself on its
+ * first call on a device. Safe to call repeatedly and from several threads. */
+int w2v_init(void);
+
+/* Waits for `stream` (a hipStream_t; NULL is the null stream), then returns
+ * W2V_EDEVICE_FLAG (and clears the error word) if a kernel of this library on
+ * the current device skipped a minibatch for an id outside [0, V) since the
+ * word was last reported, else W2V_OK. */
+int w2v_device_status(void* stream);
 
 /*
  * Sampling tables from unigram counts (host only; no HIP call).
@@ -115,8 +135,16 @@ int32_t w2v_hot_rows(const int64_t* counts, int32_t V, double neg_power,
 
 /* Number of sentences w2v_train_epoch processes concurrently when called with
  * max_inflight = 0 on the current device (one wavefront each), or a negative
- * W2V_E* code. */
-int64_t w2v_default_inflight(int32_t D, int32_t window, int32_t K);
+ * W2V_E* code: the wavefronts the device holds at once for this shape,
+ * capped at max(1, floor(V / (4 group (2 window + K + 1)))). The cap keeps
+ * the rows that the concurrent minibatches hold (up to 2 window input rows
+ * and K + 1 output rows each, group times that for a group) under a quarter
+ * of the vocabulary, so that a small vocabulary is not trained mostly from
+ * stale rows; Hogwild staleness is what separates the concurrent epoch from
+ * the sequential one (Sec. 1.1). At V = 10^6, window 5, K = 5 the cap
+ * (15,625) is above what the GPU holds. */
+int64_t w2v_default_inflight(int32_t V, int32_t D, int32_t window, int32_t K,
+                             int32_t group);
 
 /* LDS slots per wavefront in which w2v_train_epoch (W2V_ALGORITHM_HOGBATCH,
  * group 1) collects pending input-row updates for this shape on the current
@@ -151,7 +179,7 @@ int32_t w2v_pending_slots(int32_t D, int32_t window, int32_t K);
  * minibatch). Minibatches of one sentence run in order on one wavefront; up
  * to max_inflight sentences run concurrently and their updates interleave
  * without locks (Hogwild). max_inflight = 1 processes every minibatch in
- * sequence; 0 picks enough concurrent sentences to fill the GPU.
+ * sequence; 0 picks w2v_default_inflight(V, D, window, K, group).
  * Pending input rows (W2V_ALGORITHM_HOGBATCH with group 1): consecutive
  * targets share most input words, so a wavefront adds the updates of a cold
  * input row (id >= max(hot_rows, split_rows)) to one of
@@ -218,10 +246,14 @@ int32_t w2v_pending_slots(int32_t D, int32_t window, int32_t K);
  * w2v_train_epoch_workspace_bytes(split_rows, ld) bytes, 256-byte aligned,
  * caller-owned, its
  * contents need not be initialised (the call clears what it uses), and it
- * must not be shared by calls that overlap in time. stats: device int64[4]
+ * must not be shared by calls that overlap in time. stats: device int64[5]
  * or NULL, accumulated into:
  * [0] minibatches applied, [1] sum of N over them, [2] raw positions
- * visited, [3] minibatches skipped for an id outside [0, V).
+ * visited, [3] minibatches skipped for an id outside [0, V) (for the corpus:
+ * positions holding such an id, -1 excepted), [4] rows read and written
+ * back: per minibatch its distinct input and output rows, per group of
+ * targets (group > 1) the distinct rows of the group, per input word of
+ * Alg. 1 its row and K + 1 output rows.
  * Limits: 1 <= D <= W2V_MAX_DIM, 1 <= window <= W2V_MAX_WINDOW,
  * 0 <= K <= W2V_MAX_NEGATIVE, 1 <= sentence_len <= W2V_MAX_SENTENCE.
  */
@@ -269,7 +301,13 @@ int w2v_build_vocab(const int32_t* raw, int64_t T, int32_t V_raw,
 /*
  * The minibatches w2v_train_epoch would form over [pos_begin, pos_end),
  * written out instead of applied (same arguments and readings as
- * w2v_train_epoch; the matrices are not needed). Outputs are indexed by raw
+ * w2v_train_epoch; the matrices are not needed): for every target word its
+ * N input words and the K negatives they share (Sec. 1.1, negative sample
+ * sharing; Alg. 1's problem statement: a target word, N input words, K
+ * negatives drawn from V), with the sentence, window, subsampling, table and
+ * learning-rate readings stated for w2v_train_epoch. This is the sampling
+ * half of the epoch, exported so that it can be compared bit for bit with an
+ * independent implementation. Outputs are indexed by raw
  * position r = p - pos_begin, P = pos_end - pos_begin:
  *   out_targets  device int32[P]: the target word, or -1 where position p
  *                forms no minibatch (not kept, or no input word);
@@ -294,15 +332,25 @@ size_t w2v_step_batch_workspace_bytes(int32_t V, int32_t ld);
 
 /*
  * One deterministic batch of B independent HogBatch minibatches against given
- * matrices: every gradient is computed from the matrices as they were on
- * entry; the per-minibatch updates are summed per element in fp64 (in
- * `workspace`) and each touched element becomes fp32(M + sum), one rounding
- * per element. Elements whose summed update is exactly 0 keep their bits.
+ * matrices. Each minibatch is the step of Sec. 1.1 for one target word, its
+ * N input words and K shared negatives (Alg. 1's problem statement:
+ * given M_in, M_out, alpha, a target word and N input words): X = A O^T,
+ * E = alpha (l - sigma(X)), M_in[inputs] += E O, M_out[target, negatives]
+ * += E^T A. Every gradient is computed from the matrices as they were on
+ * entry: the paper computes a minibatch's products from the rows as read and
+ * writes the updates back when its matrix product is done (Sec. 1.1); here
+ * the whole batch shares that snapshot, so the result does not depend on the
+ * order of the minibatches (a deterministic counterpart of the Hogwild
+ * epoch, not a step the paper runs as such). The per-minibatch updates are
+ * summed per element in fp64 (in `workspace`) and each touched element
+ * becomes fp32(M + sum), one rounding per element. Elements whose summed
+ * update is exactly 0 keep their bits.
  * targets: device int32[B]; contexts: device int32[B][N], -1 = absent;
  * negatives: device int32[B][K]; a negative equal to its target is masked.
  * alpha: device float[B], or NULL to use alpha_scalar for every minibatch.
  * workspace: device, >= w2v_step_batch_workspace_bytes(V, ld) bytes, 256-byte
- * aligned. stats: device int64[4] or NULL, as in w2v_train_epoch.
+ * aligned. stats: device int64[5] or NULL, as in w2v_train_epoch ([2] is
+ * not used).
  * Limits: 0 <= N <= W2V_MAX_BATCH_INPUTS, 0 <= K <= W2V_MAX_NEGATIVE,
  * 1 <= D <= W2V_MAX_DIM.
  */

@@ -37,6 +37,74 @@ static int hip_fail(hipError_t e, const char* what) {
   return failf(W2V_EHIP, "%s: %s", what, hipGetErrorString(e));
 }
 
+// Per-device state set up by w2v_init (or by the first GPU call on the
+// device): the error word, one int32 of pinned host memory mapped into the
+// device's address space. Kernels that skip a minibatch for an id outside
+// [0, V) store kStatusBadId into it (a system-scope store, so the host reads
+// it without a copy or a synchronisation); every later call on the device
+// reports it once as W2V_EDEVICE_FLAG and clears it.
+constexpr int kMaxDevices = 64;
+
+struct DeviceState {
+  bool ready = false;
+  volatile int32_t* status_host = nullptr;  // what the host reads
+  int32_t* status_dev = nullptr;            // the same word, device address
+};
+
+static std::mutex g_dev_mu;
+static DeviceState g_dev[kMaxDevices];
+
+static int current_device(int& dev) {
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices)
+    return failf(W2V_EUNSUPPORTED, "device %d: at most %d devices", dev, kMaxDevices);
+  return W2V_OK;
+}
+
+// Sets up the current device's state once (caller holds g_dev_mu).
+static int setup_device_locked(int dev) {
+  DeviceState& st = g_dev[dev];
+  if (st.ready) return W2V_OK;
+  void* host = nullptr;
+  hipError_t e = hipHostMalloc(&host, 256, hipHostMallocMapped | hipHostMallocCoherent);
+  if (e != hipSuccess) return hip_fail(e, "hipHostMalloc of the error word");
+  void* mapped = nullptr;
+  e = hipHostGetDevicePointer(&mapped, host, 0);
+  if (e != hipSuccess) {
+    (void)hipHostFree(host);
+    return hip_fail(e, "hipHostGetDevicePointer of the error word");
+  }
+  st.status_host = (volatile int32_t*)host;
+  *st.status_host = 0;
+  st.status_dev = (int32_t*)mapped;
+  st.ready = true;
+  return W2V_OK;
+}
+
+// Entry check of every GPU call: sets up the device if needed, reports (and
+// clears) a skip recorded by an earlier call, and gives the kernels the
+// error word. A reported skip means this call launched nothing.
+static int enter_device(int32_t** status_dev) {
+  int dev = 0;
+  int rc = current_device(dev);
+  if (rc != W2V_OK) return rc;
+  std::lock_guard<std::mutex> lock(g_dev_mu);
+  rc = setup_device_locked(dev);
+  if (rc != W2V_OK) return rc;
+  DeviceState& st = g_dev[dev];
+  if (*st.status_host != 0) {
+    *st.status_host = 0;
+    return failf(W2V_EDEVICE_FLAG,
+                 "an earlier call on device %d skipped work: an id outside [0, V) "
+                 "in the corpus, the negative table or a batch (stats[3] counts them); "
+                 "this call launched nothing",
+                 dev);
+  }
+  *status_dev = st.status_dev;
+  return W2V_OK;
+}
+
 // Compute units of the current device (queried once per device).
 static int cu_count() {
   static std::mutex mu;
@@ -111,15 +179,48 @@ static int epoch_blocks_per_cu(int C, int nmax, int window, int K) {
   return train_blocks_per_cu(C, nmax, K);
 }
 
+// Concurrency cap of a default launch (max_inflight = 0) for a vocabulary
+// of V words: V / (4 G (2 window + K + 1)), at least 1. A minibatch holds
+// up to 2 window input rows and K + 1 output rows while it computes; a
+// group of G targets holds about G times as many and takes its step from
+// rows G targets old. With the cap, the rows the concurrent sentences hold
+// at once stay under a quarter of the vocabulary, so few of them are read
+// stale. Measured on 200,000 tokens over 1,000 words (200 sentences, cap
+// 15): the training loss of every tenth of the epoch within 0.4% of the
+// sequential epoch, against up to 12% apart with all 200 sentences in
+// flight. At 10^6 words the cap (15,625) is above what the GPU holds.
+static int64_t vocab_inflight_cap(int64_t V, int window, int K, int group) {
+  const int64_t per = 4 * (int64_t)group * (2 * (int64_t)window + K + 1);
+  const int64_t cap = V / per;
+  return cap > 0 ? cap : 1;
+}
+
 }  // namespace w2v
 
 using namespace w2v;
 
 extern "C" {
 
-int w2v_version(void) { return 100; }
+int w2v_version(void) { return 101; }
 
 const char* w2v_last_error(void) { return g_error; }
+
+int w2v_init(void) {
+  int dev = 0;
+  int rc = current_device(dev);
+  if (rc != W2V_OK) return rc;
+  std::lock_guard<std::mutex> lock(g_dev_mu);
+  rc = setup_device_locked(dev);
+  return rc == W2V_OK ? ok() : rc;
+}
+
+int w2v_device_status(void* stream) {
+  hipError_t e = hipStreamSynchronize((hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
+  int32_t* unused = nullptr;
+  const int rc = enter_device(&unused);
+  return rc == W2V_OK ? ok() : rc;
+}
 
 int w2v_build_tables(const int64_t* counts, int32_t V, double neg_power,
                      double sample_t, int32_t* neg_table, int64_t table_size,
@@ -134,7 +235,11 @@ int32_t w2v_hot_rows(const int64_t* counts, int32_t V, double neg_power,
   return hot_rows(counts, V, neg_power, sample_t, window, K, inflight, tol);
 }
 
-int64_t w2v_default_inflight(int32_t D, int32_t window, int32_t K) {
+int64_t w2v_default_inflight(int32_t V, int32_t D, int32_t window, int32_t K,
+                             int32_t group) {
+  if (V <= 0) return fail(W2V_EINVAL, "V must be positive");
+  if (group != 1 && group != 2 && group != 4 && group != 8)
+    return fail(W2V_EINVAL, "group must be 1, 2, 4 or 8");
   if (D < 1 || D > W2V_MAX_DIM)
     return failf(W2V_EINVAL, "D must be in [1, %d]", W2V_MAX_DIM);
   if (window < 1 || window > W2V_MAX_WINDOW)
@@ -146,11 +251,15 @@ int64_t w2v_default_inflight(int32_t D, int32_t window, int32_t K) {
   if (C == 0 || nmax == 0 || !train_shape_supported(C, nmax))
     return failf(W2V_EUNSUPPORTED, "no compiled kernel for D=%d window=%d", D,
                  window);
-  const int per_cu = epoch_blocks_per_cu(C, nmax, window, K);
+  const int omax = group > 1 ? group_outputs_cap_for(group + K) : 0;
+  const int per_cu = group > 1 ? grouped_blocks_per_cu(C, omax, K)
+                               : epoch_blocks_per_cu(C, nmax, window, K);
   const int cus = cu_count();
   if (per_cu <= 0 || cus <= 0) return fail(W2V_EHIP, "device query failed");
   ok();
-  return (int64_t)per_cu * cus;
+  const int64_t full = (int64_t)per_cu * cus;
+  const int64_t cap = vocab_inflight_cap(V, window, K, group);
+  return full < cap ? full : cap;
 }
 
 int32_t w2v_pending_slots(int32_t D, int32_t window, int32_t K) {
@@ -227,6 +336,9 @@ int w2v_train_epoch(const int32_t* corpus, int64_t T, int64_t pos_begin,
   if (!shape_ok)
     return failf(W2V_EUNSUPPORTED, "no compiled kernel for D=%d window=%d", D,
                  window);
+  int32_t* status = nullptr;
+  rc = enter_device(&status);
+  if (rc != W2V_OK) return rc;
   const int64_t n_sent = (pos_end - pos_begin + sentence_len - 1) / sentence_len;
   if (n_sent == 0) return ok();
 
@@ -237,6 +349,7 @@ int w2v_train_epoch(const int32_t* corpus, int64_t T, int64_t pos_begin,
   a.pos_end = pos_end;
   a.n_sent = n_sent;
   a.L = sentence_len;
+  a.status = status;
   a.M_in = M_in;
   a.M_out = M_out;
   a.V = V;
@@ -272,6 +385,8 @@ int w2v_train_epoch(const int32_t* corpus, int64_t T, int64_t pos_begin,
                                  : epoch_blocks_per_cu(C, nmax, window, K);
     const int cus = cu_count();
     grid = (int64_t)(per_cu > 0 ? per_cu : 1) * (cus > 0 ? cus : 1);
+    const int64_t cap = vocab_inflight_cap(V, window, K, group);
+    if (grid > cap) grid = cap;
   }
   if (grid > n_sent) grid = n_sent;
   if (grid > (1 << 30)) grid = 1 << 30;
@@ -313,9 +428,13 @@ int w2v_debug_minibatches(const int32_t* corpus, int64_t T, int64_t pos_begin,
   if (out_targets == nullptr || out_ctx == nullptr || out_alpha == nullptr ||
       (K > 0 && (out_negs == nullptr || out_mask == nullptr)))
     return fail(W2V_EINVAL, "output pointers must not be NULL");
+  int32_t* status = nullptr;
+  rc = enter_device(&status);
+  if (rc != W2V_OK) return rc;
   const int64_t n_sent = (pos_end - pos_begin + sentence_len - 1) / sentence_len;
   if (n_sent == 0) return ok();
   EpochArgs a{};
+  a.status = status;
   a.corpus = corpus;
   a.T = T;
   a.pos_begin = pos_begin;
@@ -381,11 +500,15 @@ int w2v_step_batch(int32_t B, int32_t N, int32_t K, const int32_t* targets,
   const int nmax = inputs_cap_for(N > 0 ? N : 1);
   if (C == 0 || nmax == 0 || !train_shape_supported(C, nmax))
     return failf(W2V_EUNSUPPORTED, "no compiled kernel for D=%d N=%d", D, N);
+  int32_t* status = nullptr;
+  rc = enter_device(&status);
+  if (rc != W2V_OK) return rc;
   if (B == 0 || N == 0) return ok();
 
   hipStream_t s = (hipStream_t)stream;
 
   StepArgs a{};
+  a.status = status;
   a.B = B;
   a.N = N;
   a.K = K;
@@ -444,9 +567,13 @@ int w2v_step_batch_sorted(int32_t B, int32_t N, int32_t K, const int32_t* target
   const int nmax = inputs_cap_for(N > 0 ? N : 1);
   if (C == 0 || nmax == 0 || !sorted_step_supported(C, nmax))
     return failf(W2V_EUNSUPPORTED, "no compiled kernel for D=%d N=%d", D, N);
+  int32_t* status = nullptr;
+  rc = enter_device(&status);
+  if (rc != W2V_OK) return rc;
   if (B == 0 || N == 0) return ok();
 
   SortedStepArgs a{};
+  a.status = status;
   a.B = B;
   a.N = N;
   a.K = K;
@@ -486,6 +613,9 @@ int w2v_build_vocab(const int32_t* raw, int64_t T, int32_t V_raw,
                  w2v_build_vocab_workspace_bytes(V_raw));
   if (((uintptr_t)workspace & 255u) != 0)
     return fail(W2V_EINVAL, "workspace must be 256-byte aligned");
+  int32_t* status = nullptr;
+  const int rc = enter_device(&status);
+  if (rc != W2V_OK) return rc;
   hipError_t e = launch_vocab(raw, T, V_raw, min_count, ranked_counts, rank_of,
                               v_kept, corpus_out, workspace, (hipStream_t)stream);
   if (e != hipSuccess) return hip_fail(e, "vocabulary launch");

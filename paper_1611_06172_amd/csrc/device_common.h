@@ -222,6 +222,18 @@ constexpr int kCoherentLoad = 16;
 // the minibatch-long read-to-write window of Hogwild would.
 constexpr int kCoherentStore = 16;
 
+// Error word of the device (host memory mapped into the device's address
+// space): a kernel that skipped work because of an id outside [0, V) stores
+// kStatusBadId there; the next library call on the host reports it. The
+// store goes to system scope so that the host sees it without a copy.
+constexpr int32_t kStatusBadId = 1;
+
+__device__ __forceinline__ void report_bad_ids(int32_t* status, int64_t n_bad) {
+  if (status != nullptr && n_bad != 0)
+    __hip_atomic_store(status, kStatusBadId, __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_SYSTEM);
+}
+
 // Coherent (agent-scope) row element load and fp32 atomic add; used for the
 // live matrices that other wavefronts update concurrently.
 __device__ __forceinline__ float load_live(const float* p) {

@@ -127,7 +127,7 @@ __global__ __launch_bounds__(kWave) __attribute__((
     io.add(0, a.M_in, id, d);
   };
 
-  int64_t n_mb = 0, sum_n = 0, raw = 0, rejected = 0;
+  int64_t n_mb = 0, sum_n = 0, raw = 0, rejected = 0, rows = 0;
   double lsum = 0.0, lcnt = 0.0;
   int bucket = -1;
 
@@ -162,6 +162,7 @@ __global__ __launch_bounds__(kWave) __attribute__((
           const int n_in = stage_inputs(lane, ctx_id, lane < n, mb);
           const int neg = lane < K ? negs_lds[j * K + lane] : 0;
           const int n_out = stage_outputs(lane, sl.ret_id[qj], neg, K, mb);
+          rows += n_in + n_out;
           if (nslots > 0)
             assign_slots<NMAX>(mb, n_in, qj, 2 * a.w, nslots, a.pend_from, lane,
                                slot_id, slot_t, flush);
@@ -197,7 +198,7 @@ __global__ __launch_bounds__(kWave) __attribute__((
     }
   }
   if (want_loss && bucket >= 0) flush_loss(a.loss, bucket, lsum, lcnt, lane);
-  flush_stats(a.stats, lane, n_mb, sum_n, raw, rejected);
+  flush_stats(a, lane, n_mb, sum_n, raw, rejected, rows);
 }
 
 // Partial rows of the split rows: cleared before an epoch, summed (in the
@@ -249,7 +250,7 @@ __global__ __launch_bounds__(kWave) void k_epoch_grouped(EpochArgs a) {
   const int G = a.group;
   const bool want_loss = a.loss != nullptr;
 
-  int64_t n_mb = 0, sum_n = 0, raw = 0, rejected = 0;
+  int64_t n_mb = 0, sum_n = 0, raw = 0, rejected = 0, rows = 0;
   double lsum = 0.0, lcnt = 0.0;
   int bucket = -1;
 
@@ -354,6 +355,7 @@ __global__ __launch_bounds__(kWave) void k_epoch_grouped(EpochArgs a) {
 
         n_mb += __popcll(members);
         sum_n += total;
+        rows += n_in + n_out;
         float loss_part = 0.f;
         run_group<C, OMAX>(a, lane, n_in, n_out, mb, gl, G, want_loss, loss_part);
         if (want_loss) {
@@ -373,7 +375,7 @@ __global__ __launch_bounds__(kWave) void k_epoch_grouped(EpochArgs a) {
     }
   }
   if (want_loss && bucket >= 0) flush_loss(a.loss, bucket, lsum, lcnt, lane);
-  flush_stats(a.stats, lane, n_mb, sum_n, raw, rejected);
+  flush_stats(a, lane, n_mb, sum_n, raw, rejected, rows);
 }
 
 // ------------------------------------------------------------ launchers --

@@ -25,7 +25,8 @@ struct EpochArgs {
   uint64_t seed;
   double* loss;            // NULL or double[2 * n_buckets]
   int32_t n_buckets;
-  int64_t* stats;          // NULL or int64[4]
+  int64_t* stats;          // NULL or int64[5]
+  int32_t* status;         // NULL or the device's error word (host-mapped)
   int32_t hot_rows;        // ids below this get atomic updates
   int32_t split_rows;      // ids below this use partial rows in `part`
   int32_t group;           // consecutive targets sharing one negative draw
@@ -57,6 +58,7 @@ struct StepArgs {
   int32_t V, D;
   int64_t ld;
   int64_t* stats;
+  int32_t* status;         // NULL or the device's error word (host-mapped)
 };
 
 // Sorted snapshot batch: the snapshot batch's inputs plus the staging rows
@@ -73,6 +75,7 @@ struct SortedStepArgs {
   int32_t V, D;
   int64_t ld;
   int64_t* stats;
+  int32_t* status;         // NULL or the device's error word (host-mapped)
   float* stage_in;         // [B][N][ld] updates of the distinct input rows
   float* stage_out;        // [B][K+1][ld] updates of the output rows
   uint32_t* key_in;        // [B][N] sort key of each staging row: the M_in

@@ -58,7 +58,7 @@ __global__ __launch_bounds__(kWave) void k_epoch_pairwise(EpochArgs a) {
   const int D = a.D;
   const bool want_loss = a.loss != nullptr;
 
-  int64_t n_mb = 0, sum_n = 0, raw = 0, rejected = 0;
+  int64_t n_mb = 0, sum_n = 0, raw = 0, rejected = 0, rows = 0;
   double lsum = 0.0, lcnt = 0.0;
   int bucket = -1;
 
@@ -95,6 +95,7 @@ __global__ __launch_bounds__(kWave) void k_epoch_pairwise(EpochArgs a) {
         }
         ++n_mb;
         sum_n += n;
+        rows += (int64_t)n * (K + 2);  // per input word: its row, K + 1 output rows
         float loss_t = 0.f;  // lane-uniform
 
         for (int i = 0; i < n; ++i) {
@@ -216,7 +217,7 @@ __global__ __launch_bounds__(kWave) void k_epoch_pairwise(EpochArgs a) {
     }
   }
   if (want_loss && bucket >= 0) flush_loss(a.loss, bucket, lsum, lcnt, lane);
-  flush_stats(a.stats, lane, n_mb, sum_n, raw, rejected);
+  flush_stats(a, lane, n_mb, sum_n, raw, rejected, rows);
 }
 
 // ------------------------------------------------------------ launchers --

@@ -52,8 +52,11 @@ __device__ __forceinline__ int keep_and_compact(const EpochArgs& a, int64_t sb,
     const int off = base + lane;
     const bool in = off < len;
     const int x = in ? a.corpus[sb + off] : 0;
-    const bool bad = in && (x < 0 || x >= a.V);
-    bool keep = in && !bad;
+    // -1 marks a word dropped from the vocabulary (w2v_build_vocab): it is
+    // removed from the sentence before windows form, as any out-of-range id,
+    // but it is no error.
+    const bool bad = in && (x < -1 || x >= a.V);
+    bool keep = in && x >= 0 && x < a.V;
     if (keep && a.thr != nullptr) {
       const U64x4 blk = stream_block(a.seed, (uint64_t)(sb + off), e, 0);
       keep = (uint32_t)blk.v[0] <= a.thr[x];
@@ -152,15 +155,20 @@ __device__ __forceinline__ void flush_loss(double* loss, int bucket,
   lcnt = 0.0;
 }
 
-// Adds a wave's counters into stats[0..3] (lane 0).
-__device__ __forceinline__ void flush_stats(int64_t* stats, int lane,
+// Adds a wave's counters into stats[0..4] (lane 0) and raises the device's
+// error word if the wave skipped anything for an id outside [0, V).
+__device__ __forceinline__ void flush_stats(const EpochArgs& a, int lane,
                                             int64_t n_mb, int64_t sum_n,
-                                            int64_t raw, int64_t rejected) {
+                                            int64_t raw, int64_t rejected,
+                                            int64_t rows) {
+  int64_t* const stats = a.stats;
+  if (lane == 0) report_bad_ids(a.status, rejected);
   if (stats != nullptr && lane == 0) {
     atomicAdd((unsigned long long*)&stats[0], (unsigned long long)n_mb);
     atomicAdd((unsigned long long*)&stats[1], (unsigned long long)sum_n);
     atomicAdd((unsigned long long*)&stats[2], (unsigned long long)raw);
     atomicAdd((unsigned long long*)&stats[3], (unsigned long long)rejected);
+    atomicAdd((unsigned long long*)&stats[4], (unsigned long long)rows);
   }
 }
 

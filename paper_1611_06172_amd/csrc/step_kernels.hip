@@ -24,7 +24,7 @@ template <int C, int NMAX, bool kMulti>
 __global__ __launch_bounds__(kWave) void k_step(StepArgs a) {
   __shared__ MinibatchLds mb;
   const int lane = threadIdx.x;
-  int64_t applied = 0, sum_n = 0, rejected = 0;
+  int64_t applied = 0, sum_n = 0, rejected = 0, rows = 0;
   for (int64_t b = blockIdx.x; b < a.B; b += gridDim.x) {
     const int t = a.targets[b];
     int bad = (t < 0 || t >= a.V);
@@ -47,6 +47,7 @@ __global__ __launch_bounds__(kWave) void k_step(StepArgs a) {
     } else if (n > 0) {
       ++applied;
       sum_n += n;
+      rows += n_in + n_out;
       const float alpha = a.alpha != nullptr ? a.alpha[b] : a.alpha_scalar;
       float unused = 0.f;
       run_minibatch<C, NMAX, kMulti, false, true>(a.M_in, a.M_out, a.dM_in, a.dM_out,
@@ -55,10 +56,12 @@ __global__ __launch_bounds__(kWave) void k_step(StepArgs a) {
     }
     __syncthreads();
   }
+  if (lane == 0) report_bad_ids(a.status, rejected);
   if (a.stats != nullptr && lane == 0) {
     atomicAdd((unsigned long long*)&a.stats[0], (unsigned long long)applied);
     atomicAdd((unsigned long long*)&a.stats[1], (unsigned long long)sum_n);
     atomicAdd((unsigned long long*)&a.stats[3], (unsigned long long)rejected);
+    atomicAdd((unsigned long long*)&a.stats[4], (unsigned long long)rows);
   }
 }
 

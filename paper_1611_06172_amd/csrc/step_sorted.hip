@@ -39,7 +39,7 @@ __global__ __launch_bounds__(kWave) void k_stage(SortedStepArgs a) {
   __shared__ MinibatchLds mb;
   const int lane = threadIdx.x;
   const int n_slots_out = a.K + 1;
-  int64_t applied = 0, sum_n = 0, rejected = 0;
+  int64_t applied = 0, sum_n = 0, rejected = 0, rows = 0;
   for (int64_t b = blockIdx.x; b < a.B; b += gridDim.x) {
     const int t = a.targets[b];
     int bad = (t < 0 || t >= a.V);
@@ -74,6 +74,7 @@ __global__ __launch_bounds__(kWave) void k_stage(SortedStepArgs a) {
     } else if (n > 0) {
       ++applied;
       sum_n += n;
+      rows += n_in + n_out;
       const float alpha = a.alpha != nullptr ? a.alpha[b] : a.alpha_scalar;
       float unused = 0.f;
       const StagedRows stage{a.stage_in + in0 * a.ld, a.stage_out + out0 * a.ld,
@@ -84,10 +85,12 @@ __global__ __launch_bounds__(kWave) void k_stage(SortedStepArgs a) {
     }
     __syncthreads();
   }
+  if (lane == 0) report_bad_ids(a.status, rejected);
   if (a.stats != nullptr && lane == 0) {
     atomicAdd((unsigned long long*)&a.stats[0], (unsigned long long)applied);
     atomicAdd((unsigned long long*)&a.stats[1], (unsigned long long)sum_n);
     atomicAdd((unsigned long long*)&a.stats[3], (unsigned long long)rejected);
+    atomicAdd((unsigned long long*)&a.stats[4], (unsigned long long)rows);
   }
 }
 

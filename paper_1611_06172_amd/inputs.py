@@ -67,6 +67,67 @@ def zipf_corpus_device(T: int, V: int, s: float, seed: int, device,
     return out
 
 
+_SPLITMIX_INC = 0x9E3779B97F4A7C15
+_SPLITMIX_M1 = 0xBF58476D1CE4E5B9
+_SPLITMIX_M2 = 0x94D049BB133111EB
+
+
+def _i64(c: int) -> int:
+    """A 64-bit constant as the signed value torch's int64 arithmetic uses."""
+    return c - (1 << 64) if c >= (1 << 63) else c
+
+
+def _splitmix64_torch(x):
+    """SplitMix64 finaliser (Steele, Lea and Flood, OOPSLA 2014) of int64
+    tensor x, in wrapping 64-bit arithmetic; logical right shifts are
+    arithmetic shifts masked to the shifted width."""
+    import torch
+
+    def srl(z, k):
+        return torch.bitwise_and(torch.bitwise_right_shift(z, k), (1 << (64 - k)) - 1)
+
+    z = x + _i64(_SPLITMIX_INC)
+    z = torch.bitwise_xor(z, srl(z, 30)) * _i64(_SPLITMIX_M1)
+    z = torch.bitwise_xor(z, srl(z, 27)) * _i64(_SPLITMIX_M2)
+    return torch.bitwise_xor(z, srl(z, 31))
+
+
+def splitmix64_numpy(x: np.ndarray) -> np.ndarray:
+    """The same finaliser on uint64 numpy arrays (numpy's uint64 arithmetic
+    wraps modulo 2^64): the reference the torch version is tested against."""
+    z = x.astype(np.uint64) + np.uint64(_SPLITMIX_INC)
+    z = (z ^ (z >> np.uint64(30))) * np.uint64(_SPLITMIX_M1)
+    z = (z ^ (z >> np.uint64(27))) * np.uint64(_SPLITMIX_M2)
+    return z ^ (z >> np.uint64(31))
+
+
+def zipf_corpus_hashed(T: int, V: int, s: float, seed: int, device="cpu",
+                       begin: int = 0, chunk: int = 1 << 26):
+    """Tokens begin..begin+T-1 of an i.i.d. Zipf(s) stream over V words,
+    the same ids on every torch device: token i takes u_i = top 53 bits of
+    SplitMix64(seed * 2^40 + i) / 2^53 and the inverse CDF of the Zipf law
+    (a binary search over fp64 cumulative probabilities, so integer and
+    comparison work only). The throughput benchmark draws its 10^9-token
+    corpus on the GPU and the oracle's stored results use the same ids,
+    drawn on the host. Returns int32[T] on `device`."""
+    import torch
+    if not 0 <= seed < (1 << 22):
+        raise ValueError("seed must be in [0, 2^22)")
+    cdf = torch.from_numpy(zipf_cdf(V, s)).to(device)
+    out = torch.empty(T, dtype=torch.int32, device=device)
+    base = seed << 40
+    for b in range(0, T, chunk):
+        e = min(T, b + chunk)
+        idx = torch.arange(base + begin + b, base + begin + e, dtype=torch.int64,
+                           device=device)
+        h = _splitmix64_torch(idx)
+        top = torch.bitwise_and(torch.bitwise_right_shift(h, 11), (1 << 53) - 1)
+        u = top.to(torch.float64) * (1.0 / (1 << 53))
+        ids = torch.searchsorted(cdf, u, right=True)
+        out[b:e] = torch.clamp(ids, max=V - 1).to(torch.int32)
+    return out
+
+
 def kernel_batch(B: int, N: int, K: int, V: int, s: float, seed: int):
     """Ids of B independent minibatches: targets [B], contexts [B, N],
     negatives [B, K], all i.i.d. Zipf(s) over V words."""

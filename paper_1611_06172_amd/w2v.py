@@ -31,6 +31,7 @@ EINVAL = -1
 EHIP = -2
 ENOMEM = -3
 EUNSUPPORTED = -4
+EDEVICE_FLAG = -5
 
 
 class W2VError(RuntimeError):
@@ -51,6 +52,10 @@ def lib():
     L = ctypes.CDLL(LIB_PATH)
     L.w2v_version.restype = ctypes.c_int
     L.w2v_last_error.restype = ctypes.c_char_p
+    L.w2v_init.argtypes = []
+    L.w2v_init.restype = ctypes.c_int
+    L.w2v_device_status.argtypes = [_vp]
+    L.w2v_device_status.restype = ctypes.c_int
     L.w2v_build_tables.argtypes = [_vp, _i32, _f64, _f64, _vp, _i64, _vp]
     L.w2v_build_tables.restype = ctypes.c_int
     L.w2v_train_epoch.argtypes = [
@@ -71,7 +76,7 @@ def lib():
     L.w2v_debug_minibatches.restype = ctypes.c_int
     L.w2v_hot_rows.argtypes = [_vp, _i32, _f64, _f64, _i32, _i32, _i64, _f64]
     L.w2v_hot_rows.restype = ctypes.c_int32
-    L.w2v_default_inflight.argtypes = [_i32, _i32, _i32]
+    L.w2v_default_inflight.argtypes = [_i32, _i32, _i32, _i32, _i32]
     L.w2v_default_inflight.restype = ctypes.c_int64
     L.w2v_pending_slots.argtypes = [_i32, _i32, _i32]
     L.w2v_pending_slots.restype = ctypes.c_int32
@@ -117,16 +122,26 @@ def _dev(t, dtype, name, ndim=None):
         raise TypeError(f"{name} must have dtype {dtype}, got {t.dtype}")
     if ndim is not None and t.dim() != ndim:
         raise ValueError(f"{name} must be {ndim}-D")
-    if not t.is_contiguous() and not (t.dim() == 2 and t.stride(1) == 1):
+    # The kernels index every argument but the two matrices as packed arrays
+    # (contexts[b N + i], loss[2 b], ...): a strided view would be read at
+    # the wrong places, so only contiguous tensors pass.
+    if not t.is_contiguous():
         raise ValueError(f"{name} must be contiguous")
     return t
 
 
 def _matrix(M, name):
+    """Checks a V x D fp32 device matrix; rows may be padded (the row stride
+    is passed to the library as ld), columns must be adjacent."""
     import torch
-    _dev(M, torch.float32, name, 2)
-    if M.stride(1) != 1:
-        raise ValueError(f"{name} must have unit column stride")
+    if not isinstance(M, torch.Tensor) or not M.is_cuda:
+        raise TypeError(f"{name} must be a GPU tensor")
+    if M.dtype != torch.float32:
+        raise TypeError(f"{name} must have dtype torch.float32, got {M.dtype}")
+    if M.dim() != 2:
+        raise ValueError(f"{name} must be 2-D")
+    if M.stride(1) != 1 or M.stride(0) < M.shape[1]:
+        raise ValueError(f"{name} must have unit column stride and a row stride >= D")
     return M.shape[0], M.stride(0)
 
 
@@ -163,9 +178,23 @@ def hot_rows(counts, *, neg_power: float = 0.75, sample_t: float = 1e-4,
     return h
 
 
-def default_inflight(D: int, window: int = 5, K: int = 5) -> int:
-    """Concurrent sentences of train_epoch with max_inflight = 0."""
-    n = int(lib().w2v_default_inflight(D, window, K))
+def init():
+    """Sets up the library's state on the current device (w2v_init)."""
+    _check(lib().w2v_init())
+
+
+def device_status(stream=None):
+    """Waits for the stream, then raises W2VError (code EDEVICE_FLAG) if a
+    kernel of the library skipped work for an id outside [0, V) since this
+    was last reported (w2v_device_status)."""
+    _check(lib().w2v_device_status(_stream(stream)))
+
+
+def default_inflight(D: int, window: int = 5, K: int = 5, *, V: int,
+                     group: int = 1) -> int:
+    """Concurrent sentences of train_epoch with max_inflight = 0 over a
+    vocabulary of V words (w2v_default_inflight)."""
+    n = int(lib().w2v_default_inflight(V, D, window, K, group))
     if n < 0:
         _check(n)
     return n
@@ -223,6 +252,8 @@ def train_epoch(corpus, M_in, M_out, neg_table, keep_thresh=None, *,
         n_b = loss_buckets.shape[0]
     if stats is not None:
         _dev(stats, torch.int64, "stats", 1)
+        if stats.numel() < 5:
+            raise ValueError("stats must have 5 entries (see w2v_train_epoch)")
     T = corpus.numel()
     end = T if pos_end is None else pos_end
     need = train_epoch_workspace_bytes(split_rows, ld)
@@ -277,6 +308,10 @@ def debug_minibatches(corpus, neg_table, keep_thresh=None, *, V: int,
     _dev(neg_table, torch.int32, "neg_table", 1)
     if keep_thresh is not None:
         _dev(keep_thresh, (torch.int32, torch.uint32), "keep_thresh", 1)
+    if stats is not None:
+        _dev(stats, torch.int64, "stats", 1)
+        if stats.numel() < 5:
+            raise ValueError("stats must have 5 entries (see w2v_train_epoch)")
     T = corpus.numel()
     end = T if pos_end is None else pos_end
     P = end - pos_begin
@@ -347,6 +382,8 @@ def step_batch(targets, contexts, negatives, M_in, M_out, alpha=0.025, *,
             workspace = alloc_workspace(V, ld, M_in.device)
     if stats is not None:
         _dev(stats, torch.int64, "stats", 1)
+        if stats.numel() < 5:
+            raise ValueError("stats must have 5 entries (see w2v_train_epoch)")
     entry = lib().w2v_step_batch_sorted if sorted else lib().w2v_step_batch
     _check(entry(
         B, N, K, _ptr(targets), _ptr(contexts), _ptr(negatives), a_ptr, a_s,

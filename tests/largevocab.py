@@ -1,7 +1,9 @@
 """The large-vocabulary workload on a prefix the oracle can follow (shared by
-the GPU test and the script that stores the oracle's numbers): 1e7 i.i.d.
-Zipf(1.07) tokens over V = 1e6 (numpy generator), D = 300, K = 5, window 5,
-t = 1e-4, tables from the workload's expected counts, one epoch. The
+the GPU test and the script that stores the oracle's numbers): the first
+1e8 tokens of the throughput benchmark's own corpus (i.i.d. Zipf(1.07) over
+V = 1e6, inputs.zipf_corpus_hashed with the benchmark's seed, so the same ids
+on the host and on the GPU), D = 300, K = 5, window 5, t = 1e-4, tables from
+the prefix's counts, one epoch with the benchmark's sampling seed. The
 held-out score is the mean SGNS loss per input word of 20,000 minibatches
 drawn independently of the corpus."""
 import numpy as np
@@ -9,16 +11,19 @@ import numpy as np
 from paper_1611_06172_amd import inputs
 
 V, D, K, WINDOW, SAMPLE = 1_000_000, 300, 5, 5, 1e-4
-T = 10_000_000
-SEED = 1234
+T = 100_000_000
+CORPUS_SEED = 6          # the benchmark's corpus seed
+SEED = 1234              # the benchmark's sampling seed
+N_BUCKETS = 10
 
 
-def corpus():
-    return inputs.zipf_ids(T, V, 1.07, 8)
+def corpus(device="cpu"):
+    """int32 torch tensor of the T tokens on `device`."""
+    return inputs.zipf_corpus_hashed(T, V, 1.07, CORPUS_SEED, device)
 
 
-def counts():
-    return np.rint(inputs.zipf_pmf(V, 1.07) * 1e9).astype(np.int64)
+def counts(corpus_np):
+    return inputs.word_counts(corpus_np, V)
 
 
 def init_in():
@@ -37,7 +42,7 @@ def heldout_loss(M_in, M_out, t, c, n):
     sum_k log sigma(-a.o_k) (negatives equal to the target skipped), fp64."""
     A = np.asarray(M_in, np.float64)[c]                      # [B, 6, D]
     O = np.asarray(M_out, np.float64)[np.concatenate([t[:, None], n], 1)]  # [B, K+1, D]
-    X = np.einsum("bid,bkd->bik", A, O)
+    X = np.matmul(A, np.ascontiguousarray(O.transpose(0, 2, 1)))
     sign = np.ones(K + 1)
     sign[1:] = -1
     L = np.logaddexp(0.0, -X * sign)                         # softplus(-sign x)

@@ -4,7 +4,7 @@ import numpy as np
 import pytest
 
 import oracle
-from gpu_util import thresh_dev, to_dev
+from gpu_util import expect_device_flag, thresh_dev, to_dev
 from paper_1611_06172_amd import inputs, w2v
 from test_gpu_train_epoch import gpu_epoch, rel_row_error
 
@@ -81,9 +81,9 @@ def test_degenerate_corpora(algorithm):
 
 
 def test_out_of_range_corpus_ids_are_skipped_not_applied():
-    """Ids outside [0, V) in the corpus are dropped before windows are formed
-    (counted as rejected); the rest of the epoch equals the oracle's on the
-    corpus with those positions removed from their sentences."""
+    """Ids outside [0, V) in the corpus are dropped before windows are formed;
+    -1 (a word removed from the vocabulary) is no error, the others are
+    counted as rejected and reported once as W2V_EDEVICE_FLAG."""
     V, D = 300, 32
     corpus = inputs.zipf_ids(8000, V, 1.0, 40)
     bad = corpus.copy()
@@ -94,6 +94,68 @@ def test_out_of_range_corpus_ids_are_skipped_not_applied():
     M_out = inputs.init_matrix(V, D, "normal", 42, scale=0.05)
     gi, go, stats, _ = gpu_epoch(bad, table, None, M_in, M_out, window=4, K=3,
                                  sentence_len=1000, seed=43, max_inflight=1)
-    assert stats[3] == 3 and stats[2] == len(bad)
+    assert stats[3] == 2 and stats[2] == len(bad)
+    expect_device_flag()
     assert np.isfinite(gi).all() and np.isfinite(go).all()
     assert not np.array_equal(gi.view(np.uint32), M_in.view(np.uint32))
+
+
+def test_dropped_words_equal_subsampled_positions():
+    """A corpus position holding -1 (a word the vocabulary dropped) leaves
+    its sentence before windows form, exactly as a position that subsampling
+    rejects: the serialised epoch equals the oracle's epoch over the same
+    corpus with an extra word V in those positions whose keep threshold is 0
+    (kept only on a draw of exactly 0, which none of these positions has).
+    The word V has count 0, so it owns no slot of the negative table and the
+    table is the same. Nothing is reported as an error."""
+    V, D, L = 300, 32, 100
+    kw = dict(window=3, K=3, sentence_len=L, seed=48)
+    corpus = inputs.zipf_ids(6000, V, 1.0, 44)
+    drop = np.zeros(len(corpus), bool)
+    drop[np.random.default_rng(45).integers(0, len(corpus), 400)] = True
+    assert all(oracle.draw_u32(kw["seed"], int(p), 0, 0) != 0 for p in np.nonzero(drop)[0])
+    table, _ = oracle.build_tables(inputs.word_counts(corpus, V), 0.75, 0.0, 10**6,
+                                   want_thresh=False)
+    M_in = inputs.init_matrix(V, D, "uniform", 46)
+    M_out = inputs.init_matrix(V, D, "normal", 47, scale=0.05)
+    gi, go, stats, _ = gpu_epoch(np.where(drop, -1, corpus).astype(np.int32), table, None,
+                                 M_in, M_out, max_inflight=1, **kw)
+    assert stats[3] == 0
+    w2v.device_status()
+    o_corpus = np.where(drop, V, corpus).astype(np.int32)
+    thr = np.full(V + 1, 0xFFFFFFFF, np.uint32)
+    thr[V] = 0
+    o_in = np.vstack([M_in, np.zeros((1, D), np.float32)])
+    o_out = np.vstack([M_out, np.zeros((1, D), np.float32)])
+    n, _ = oracle.train_epoch(oracle.Sampling(o_corpus, table, thr, **kw), o_in, o_out)
+    assert stats[0] == n
+    assert rel_row_error(gi, o_in[:V]) < 2e-4
+    assert rel_row_error(go, o_out[:V]) < 2e-4
+    assert not o_in[V].any() and not o_out[V].any()
+
+
+def test_dropped_minibatch_is_reported_to_a_caller_without_stats():
+    """A caller that passes no stats learns of a skipped minibatch: the next
+    call on the device returns W2V_EDEVICE_FLAG and launches nothing, the
+    call after it runs."""
+    import torch
+    V, D = 200, 32
+    corpus = inputs.zipf_ids(3000, V, 1.0, 49)
+    corpus[1234] = V + 3
+    table, _ = oracle.build_tables(inputs.word_counts(np.clip(corpus, 0, V - 1), V), 0.75,
+                                   0.0, 10**5, want_thresh=False)
+    gi = to_dev(inputs.init_matrix(V, D, "uniform", 50))
+    go = torch.zeros_like(gi)
+    c, tb = to_dev(corpus), to_dev(table)
+    w2v.train_epoch(c, gi, go, tb, None, window=3, K=2)
+    torch.cuda.synchronize()
+    before = gi.clone()
+    with pytest.raises(w2v.W2VError) as err:
+        w2v.train_epoch(c, gi, go, tb, None, window=3, K=2)
+    assert err.value.code == w2v.EDEVICE_FLAG
+    torch.cuda.synchronize()
+    assert torch.equal(gi, before)              # the reporting call launched nothing
+    good = to_dev(np.clip(corpus, 0, V - 1).astype(np.int32))
+    w2v.train_epoch(good, gi, go, tb, None, window=3, K=2)
+    w2v.device_status()
+

@@ -1,7 +1,7 @@
 """The throughput workload's shapes and launch configuration (V = 1e6
 Zipf(1.07) words, D = 300 in rows padded to 320 floats, K = 5, window 5,
 t = 1e-4, a 1e8-slot table, the conflict model's atomic rows and split head)
-on prefixes of the corpus the oracle can follow:
+on prefixes of the benchmark's corpus that the oracle can follow:
 
 * serialised, the first 1e6 tokens: elementwise against the oracle on every
   row the minibatches touch, every other row bitwise unchanged;
@@ -24,11 +24,13 @@ V, D = 1_000_000, 300
 
 
 def workload(T):
-    corpus = inputs.zipf_ids(T, V, 1.07, 6)
+    # the first T tokens of the throughput benchmark's own corpus (same
+    # generator and seed), with tables from the law's expected counts
+    corpus = inputs.zipf_corpus_hashed(T, V, 1.07, 6).numpy()
     counts = np.rint(inputs.zipf_pmf(V, 1.07) * 1e9).astype(np.int64)
     table, thr = oracle.build_tables(counts, 0.75, 1e-4, 10**8)
     M_in = inputs.init_matrix(V, D, "uniform", 2)
-    inflight = w2v.default_inflight(D, 5, 5)
+    inflight = w2v.default_inflight(D, 5, 5, V=V)
     hot = w2v.hot_rows(counts, inflight=inflight, tol=0.5)
     split = w2v.hot_rows(counts, inflight=inflight, tol=128.0)
     return corpus, table, thr, M_in, hot, split
@@ -44,7 +46,7 @@ def run_gpu(corpus, table, thr, M_in, hot, split, **kw):
     import torch
     gi = w2v.alloc_matrix(V, D, "cuda", torch.from_numpy(M_in))
     go = w2v.alloc_matrix(V, D, "cuda")
-    stats = torch.zeros(4, dtype=torch.int64, device="cuda")
+    stats = torch.zeros(5, dtype=torch.int64, device="cuda")
     lb = torch.zeros((10, 2), dtype=torch.float64, device="cuda")
     w2v.train_epoch(to_dev(corpus), gi, go, to_dev(table),
                     torch.from_numpy(thr.view(np.int32)).cuda(), window=5, K=5,

@@ -11,7 +11,7 @@ import pytest
 import oracle
 from gpu_util import thresh_dev, to_dev
 from paper_1611_06172_amd import inputs, w2v
-from test_gpu_train_epoch import eval_loss, rel_row_error, tiny_config
+from test_gpu_train_epoch import eval_loss, gpu_epoch, heldout_batch, rel_row_error, tiny_config
 
 pytestmark = pytest.mark.gpu
 
@@ -40,7 +40,7 @@ def test_serialised_grouped_matches_oracle(G, V, D, window, K, sub, L, hot, spli
         go = w2v.alloc_matrix(V, D, "cuda", torch.from_numpy(M_out))
     else:
         gi, go = to_dev(M_in), to_dev(M_out)
-    stats = torch.zeros(4, dtype=torch.int64, device="cuda")
+    stats = torch.zeros(5, dtype=torch.int64, device="cuda")
     lb = torch.zeros((3, 2), dtype=torch.float64, device="cuda")
     w2v.train_epoch(to_dev(corpus), gi, go, to_dev(table), thresh_dev(thr), loss_buckets=lb,
                     stats=stats, max_inflight=1, hot_rows=hot, split_rows=split, group=G,
@@ -57,11 +57,54 @@ def test_serialised_grouped_matches_oracle(G, V, D, window, K, sub, L, hot, spli
 
 
 @pytest.mark.parametrize("G", [2, 4])
+def test_grouped_tiny_configuration_default_launch_trajectory(G):
+    """The tiny configuration (200,000 tokens over 1,000 words, D = 64,
+    window 5, K = 5, one epoch) with groups of G targets, launched by
+    default: the library caps the concurrent sentences at V / (4 G (2 window
+    + K + 1)) (7 for G = 2, 3 for G = 4), because a group's step reads rows
+    G targets old and so multiplies the staleness of concurrency. The
+    training loss per input word in ten buckets of raw position and the
+    held-out loss within 2% of the sequential grouped oracle's."""
+    V, D = 1000, 64
+    corpus, table, M_in, M_out = tiny_config(V=V, D=D)
+    assert w2v.default_inflight(D, 5, 5, V=V, group=G) == V // (4 * G * 16)
+    kw = dict(window=5, K=5, sentence_len=1000, seed=55, alpha0=0.025, n_epochs=1)
+    o_in, o_out = M_in.copy(), M_out.copy()
+    _, ob = oracle.grouped_train_epoch(oracle.Sampling(corpus, table, None, **kw), G,
+                                       o_in, o_out, n_buckets=10)
+    gi, go, _, gb = gpu_epoch(corpus, table, None, M_in, M_out, n_buckets=10, group=G,
+                              **kw)
+    np.testing.assert_array_equal(gb[:, 1], ob[:, 1])
+    traj_o, traj_g = ob[:, 0] / ob[:, 1], gb[:, 0] / gb[:, 1]
+    print(f"[grouped default] G={G}: buckets "
+          f"{np.round(100 * (traj_g / traj_o - 1), 2).tolist()} %", flush=True)
+    assert np.all(np.abs(traj_g - traj_o) <= 0.02 * traj_o), (traj_g, traj_o)
+    hb = heldout_batch(V, table)
+    lo, lg = eval_loss(o_in, o_out, *hb), eval_loss(gi, go, *hb)
+    assert abs(lg - lo) <= 0.02 * lo, (lg, lo)
+
+
+def test_stress_grouped_small_vocabulary_many_in_flight():
+    """Stress test, outside the statistical bar: G = 4 over 1,000 words with
+    64 sentences in flight (21 times the default concurrency for this
+    vocabulary). Observed: epoch-0 training loss 17% above the sequential
+    grouped epoch. Checked here: the run stays finite and learns."""
+    V, D = 1000, 64
+    corpus, table, M_in, M_out = tiny_config(V=V, D=D)
+    kw = dict(window=5, K=5, sentence_len=1000, seed=55, alpha0=0.025, n_epochs=1)
+    gi, go, _, gb = gpu_epoch(corpus, table, None, M_in, M_out, n_buckets=10, group=4,
+                              max_inflight=64, **kw)
+    assert np.isfinite(gi).all() and np.isfinite(go).all()
+    traj = gb[:, 0] / gb[:, 1]
+    assert traj[-1] < 0.9 * traj[0]
+    hb = heldout_batch(V, table)
+    assert eval_loss(gi, go, *hb) < 0.95 * eval_loss(M_in, M_out, *hb)
+
+
+@pytest.mark.parametrize("G", [2, 4])
 def test_hogwild_grouped_near_sequential(G):
-    """64 sentences in flight over 20,000 words (observed within 0.5%). Over
-    1,000 words the group snapshot amplifies staleness with concurrency
-    (G = 4 at 64 in flight: +17% training loss in epoch 0, +0.3% at 16), so
-    that vocabulary is not used here."""
+    """64 sentences in flight over 20,000 words, three epochs (observed
+    within 0.5%)."""
     import torch
     V = 20_000
     corpus, table, M_in, M_out = tiny_config(T=400_000, V=V)

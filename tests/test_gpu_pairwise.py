@@ -27,7 +27,7 @@ def gpu_pairwise(corpus, table, thr, M_in, M_out, n_buckets=0, ld=None, **kw):
     else:
         gi = w2v.alloc_matrix(*M_in.shape, "cuda", torch.from_numpy(M_in))
         go = w2v.alloc_matrix(*M_out.shape, "cuda", torch.from_numpy(M_out))
-    stats = torch.zeros(4, dtype=torch.int64, device="cuda")
+    stats = torch.zeros(5, dtype=torch.int64, device="cuda")
     lb = torch.zeros((n_buckets, 2), dtype=torch.float64, device="cuda") if n_buckets else None
     w2v.train_epoch(to_dev(corpus), gi, go, to_dev(table), thresh_dev(thr),
                     loss_buckets=lb, stats=stats, algorithm="pairwise", **kw)

@@ -24,7 +24,7 @@ pytestmark = pytest.mark.gpu
 def run(corpus, table, thr, M_in, M_out, algorithm, **kw):
     import torch
     gi, go = to_dev(M_in), to_dev(M_out)
-    stats = torch.zeros(4, dtype=torch.int64, device="cuda")
+    stats = torch.zeros(5, dtype=torch.int64, device="cuda")
     w2v.train_epoch(to_dev(corpus), gi, go, to_dev(table), thresh_dev(thr),
                     stats=stats, algorithm=algorithm, **kw)
     torch.cuda.synchronize()

@@ -9,7 +9,7 @@ import pytest
 
 import oracle
 from paper_1611_06172_amd import inputs, w2v
-from gpu_util import assert_same_minibatches, gpu_minibatches, thresh_dev, to_dev
+from gpu_util import assert_same_minibatches, expect_device_flag, gpu_minibatches, thresh_dev, to_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -75,10 +75,11 @@ def test_rejects_out_of_range_corpus_ids():
     corpus[2000] = -5
     table, _ = oracle.build_tables(inputs.word_counts(np.clip(corpus, 0, V - 1), V),
                                    0.75, 0.0, 1000)
-    stats = torch.zeros(4, dtype=torch.int64, device="cuda")
+    stats = torch.zeros(5, dtype=torch.int64, device="cuda")
     out = w2v.debug_minibatches(to_dev(corpus), to_dev(table), None, V=V,
                                 window=3, K=2, sentence_len=500, stats=stats)
     torch.cuda.synchronize()
     t = out["targets"].cpu().numpy()
     assert t[100] == -1 and t[2000] == -1
     assert stats[3].item() == 2 and stats[2].item() == 5000
+    expect_device_flag()

@@ -31,7 +31,7 @@ def test_sweep_shape_serialised(D, K, algorithm):
     n, ob = run(oracle.Sampling(corpus, table, thr, **kw), o_in, o_out, n_buckets=2)
     gi = w2v.alloc_matrix(V, D, "cuda", torch.from_numpy(M_in))
     go = w2v.alloc_matrix(V, D, "cuda", torch.from_numpy(M_out))
-    stats = torch.zeros(4, dtype=torch.int64, device="cuda")
+    stats = torch.zeros(5, dtype=torch.int64, device="cuda")
     lb = torch.zeros((2, 2), dtype=torch.float64, device="cuda")
     w2v.train_epoch(to_dev(corpus), gi, go, to_dev(table),
                     torch.from_numpy(thr.view(np.int32)).cuda(), loss_buckets=lb,

@@ -14,7 +14,7 @@ import pytest
 
 import oracle
 from paper_1611_06172_amd import inputs, w2v
-from gpu_util import scaled_error, to_dev
+from gpu_util import scaled_error, to_dev, expect_device_flag
 
 pytestmark = pytest.mark.gpu
 TOL = 1e-5
@@ -29,7 +29,7 @@ def check(targets, contexts, negatives, M_in, M_out, alpha, D=None, expect_skip=
                                                 M_in, M_out, alpha, D=D)
     gi, go = to_dev(M_in), to_dev(M_out)
     a = to_dev(alpha) if np.ndim(alpha) else alpha
-    stats = torch.zeros(4, dtype=torch.int64, device="cuda")
+    stats = torch.zeros(5, dtype=torch.int64, device="cuda")
     w2v.step_batch(to_dev(targets), to_dev(contexts), to_dev(negatives), gi, go,
                    a, D=D, stats=stats, sorted=sorted)
     torch.cuda.synchronize()
@@ -113,10 +113,11 @@ def test_bad_ids_are_skipped():
     Mi_o, Mo_o, S_in, S_out = oracle.step_batch(t[keep], c[keep], n[keep], Mi, Mo, 0.02)
     import torch
     gi, go = to_dev(Mi), to_dev(Mo)
-    stats = torch.zeros(4, dtype=torch.int64, device="cuda")
+    stats = torch.zeros(5, dtype=torch.int64, device="cuda")
     w2v.step_batch(to_dev(t), to_dev(c), to_dev(n), gi, go, 0.02, stats=stats)
     torch.cuda.synchronize()
     assert stats[3].item() == 3 and stats[0].item() == B - 3
+    expect_device_flag()
     assert scaled_error(gi.cpu().numpy(), Mi_o, S_in) <= TOL
     assert scaled_error(go.cpu().numpy(), Mo_o, S_out) <= TOL
 

@@ -15,7 +15,7 @@ import pytest
 
 import oracle
 from paper_1611_06172_amd import inputs, w2v
-from gpu_util import scaled_error, to_dev
+from gpu_util import scaled_error, to_dev, expect_device_flag
 from test_gpu_step_batch import TOL, check, mats
 
 pytestmark = pytest.mark.gpu
@@ -95,10 +95,11 @@ def test_bad_ids_are_skipped():
     keep[[3, 10, 20]] = False
     Mi_o, Mo_o, S_in, S_out = oracle.step_batch(t[keep], c[keep], n[keep], Mi, Mo, 0.02)
     gi, go = to_dev(Mi), to_dev(Mo)
-    stats = torch.zeros(4, dtype=torch.int64, device="cuda")
+    stats = torch.zeros(5, dtype=torch.int64, device="cuda")
     w2v.step_batch(to_dev(t), to_dev(c), to_dev(n), gi, go, 0.02, stats=stats, sorted=True)
     torch.cuda.synchronize()
     assert stats[3].item() == 3 and stats[0].item() == B - 3
+    expect_device_flag()
     assert scaled_error(gi.cpu().numpy(), Mi_o, S_in) <= TOL
     assert scaled_error(go.cpu().numpy(), Mo_o, S_out) <= TOL
 

@@ -32,7 +32,7 @@ def tiny_config(T=200_000, V=1000, D=64, seed=1):
 def gpu_epoch(corpus, table, thr, M_in, M_out, n_buckets=0, **kw):
     import torch
     gi, go = to_dev(M_in), to_dev(M_out)
-    stats = torch.zeros(4, dtype=torch.int64, device="cuda")
+    stats = torch.zeros(5, dtype=torch.int64, device="cuda")
     lb = torch.zeros((n_buckets, 2), dtype=torch.float64, device="cuda") if n_buckets else None
     w2v.train_epoch(to_dev(corpus), gi, go, to_dev(table), thresh_dev(thr),
                     loss_buckets=lb, stats=stats, **kw)
@@ -160,28 +160,90 @@ def eval_loss(M_in, M_out, t, c, n):
     return total / cnt
 
 
-@pytest.mark.parametrize("update_path,inflight,bound,algorithm", [
-    ("atomic", 64, 0.02, "hogbatch"), ("split", 64, 0.02, "hogbatch"),
-    ("model", 64, 0.02, "hogbatch"), ("model", 64, 0.02, "hogbatch_immediate"),
-    ("atomic", 0, 0.05, "hogbatch"), ("split", 0, 0.05, "hogbatch"),
-    ("atomic", 0, 0.05, "hogbatch_immediate")])
-def test_hogwild_epochs_near_sequential(update_path, inflight, bound, algorithm):
-    """Three concurrent epochs against the sequential oracle's: 64 sentences
-    in flight over 1,000 words (every row contended: all atomic, optionally
-    the head split into partial rows) or over 20,000 words with the conflict
-    model's plain rows, within 2%; all 200 sentences at once over 1,000
-    words, where staleness is extreme, within 5% (observed: about 1%).
-    Compared: the training-loss trajectory (mean loss per input word of each
-    epoch, as the minibatches were applied) and the held-out loss of the
-    final model. With the whole corpus in flight, every sentence of epoch 0
-    starts from the initial model, so that epoch's training loss is not
-    comparable (observed 9% above the sequential one) and the trajectory is
-    compared from epoch 1. Loss by raw position inside one epoch is not compared: the
-    concurrent schedule visits the sentences of a position range at other
-    model states than the sequential one. The default kernel holds the
-    updates of cold input rows back while their word is in the window, which
-    delays what other sentences see of them; the kernel that applies every
-    update at once runs two tiers beside it."""
+def heldout_batch(V, table):
+    """2,000 held-out minibatches from the corpus's unigram law."""
+    t, ctx, _ = inputs.kernel_batch(2000, 6, 5, V, 1.0, 99)
+    negs = table[np.random.default_rng(98).integers(0, len(table), (2000, 5))]
+    return t, ctx, negs
+
+
+@pytest.mark.parametrize("update_path,algorithm", [
+    ("atomic", "hogbatch"), ("split", "hogbatch"), ("atomic", "hogbatch_immediate")])
+def test_tiny_configuration_default_launch_trajectory(update_path, algorithm):
+    """The tiny configuration (200,000 i.i.d. Zipf(1.0) tokens over 1,000
+    words, D = 64, window 5, K = 5, no subsampling, one epoch, M_out = 0) as
+    the library launches it by default (max_inflight = 0, which caps the
+    concurrent sentences at V / (4 (2 window + K + 1)) = 15 for this
+    vocabulary): the training loss per input word in each of ten buckets of
+    raw position, and the held-out loss of the trained model, within 2% of
+    the sequential oracle's epoch. Counts are exact. Every row is atomic
+    (the binding's default) or the head is split into partial rows."""
+    import torch
+    V, D = 1000, 64
+    corpus, table, M_in, M_out = tiny_config(V=V, D=D)
+    assert w2v.default_inflight(D, 5, 5, V=V) == 15
+    kw = dict(window=5, K=5, sentence_len=1000, seed=7, alpha0=0.025, n_epochs=1)
+    split = 0
+    if update_path == "split":
+        split = w2v.hot_rows(inputs.word_counts(corpus, V), sample_t=0.0, inflight=15,
+                             tol=2.0)
+        assert 0 < split < 50
+    o_in, o_out = M_in.copy(), M_out.copy()
+    n, ob = oracle.train_epoch(oracle.Sampling(corpus, table, None, **kw), o_in, o_out,
+                               n_buckets=10)
+    gi, go, stats, gb = gpu_epoch(corpus, table, None, M_in, M_out, n_buckets=10,
+                                  split_rows=split, algorithm=algorithm, **kw)
+    assert stats[0] == n
+    np.testing.assert_array_equal(gb[:, 1], ob[:, 1])
+    traj_o, traj_g = ob[:, 0] / ob[:, 1], gb[:, 0] / gb[:, 1]
+    print(f"[tiny default] {update_path} {algorithm}: buckets "
+          f"{np.round(100 * (traj_g / traj_o - 1), 2).tolist()} %", flush=True)
+    assert traj_o[-1] < 0.85 * traj_o[0]
+    assert np.all(np.abs(traj_g - traj_o) <= 0.02 * traj_o), (traj_g, traj_o)
+    hb = heldout_batch(V, table)
+    lo, lg = eval_loss(o_in, o_out, *hb), eval_loss(gi, go, *hb)
+    assert lo < 0.9 * eval_loss(M_in, M_out, *hb)
+    assert abs(lg - lo) <= 0.02 * lo, (lg, lo)
+
+
+@pytest.mark.parametrize("algorithm", ["hogbatch", "hogbatch_immediate"])
+def test_stress_whole_tiny_corpus_in_flight(algorithm):
+    """Stress test, outside the statistical bar: all 200 sentences of the
+    tiny corpus in flight at once (max_inflight = 200, every row atomic), so
+    that every minibatch of a sentence's first targets starts from the
+    initial model and the 1,000 rows are updated by up to 200 concurrent
+    minibatches. Observed: training loss by tenth of the epoch 12% below to
+    7% above the sequential epoch (the concurrent schedule visits a tenth's
+    sentences at other model states; with every sentence in flight each
+    tenth's loss is close to the epoch's mean), held-out loss 0.6-1.4% above.
+    Checked here: the run stays finite and learns (the epoch's training loss
+    well below the initial (K + 1) ln 2 per input word, held-out loss down
+    by a tenth)."""
+    V, D = 1000, 64
+    corpus, table, M_in, M_out = tiny_config(V=V, D=D)
+    kw = dict(window=5, K=5, sentence_len=1000, seed=7, alpha0=0.025, n_epochs=1)
+    gi, go, stats, gb = gpu_epoch(corpus, table, None, M_in, M_out, n_buckets=10,
+                                  max_inflight=200, algorithm=algorithm, **kw)
+    assert np.isfinite(gi).all() and np.isfinite(go).all()
+    assert gb[:, 0].sum() / gb[:, 1].sum() < 0.8 * 6 * math.log(2)
+    hb = heldout_batch(V, table)
+    assert eval_loss(gi, go, *hb) < 0.9 * eval_loss(M_in, M_out, *hb)
+
+
+@pytest.mark.parametrize("update_path,algorithm", [
+    ("atomic", "hogbatch"), ("split", "hogbatch"),
+    ("model", "hogbatch"), ("model", "hogbatch_immediate")])
+def test_hogwild_epochs_near_sequential(update_path, algorithm):
+    """Three concurrent epochs with 64 sentences in flight against the
+    sequential oracle's, within 2%: over 1,000 words (every row contended:
+    all atomic, optionally the head split into partial rows) or over 20,000
+    words with the conflict model's plain rows. Compared: the training loss
+    per input word of each epoch (as the minibatches were applied) and the
+    held-out loss of the final model. The default kernel holds the updates
+    of cold input rows back while their word is in the window, which delays
+    what other sentences see of them; the kernel that applies every update
+    at once runs beside it."""
+    inflight, bound = 64, 0.02
     import torch
     V = 20_000 if update_path == "model" else 1000
     corpus, table, M_in, M_out = tiny_config(T=200_000 if V == 1000 else 400_000, V=V)
@@ -212,8 +274,7 @@ def test_hogwild_epochs_near_sequential(update_path, inflight, bound, algorithm)
         traj_g.append(gb[0, 0] / gb[0, 1])
     traj_o, traj_g = np.array(traj_o), np.array(traj_g)
     assert traj_o[-1] < traj_o[0]                       # training moved the loss
-    first = 1 if inflight == 0 else 0
-    assert np.all(np.abs(traj_g - traj_o)[first:] <= bound * traj_o[first:]), (traj_g, traj_o)
+    assert np.all(np.abs(traj_g - traj_o) <= bound * traj_o), (traj_g, traj_o)
     # held-out evaluation minibatches from the same unigram law
     t, ctx, _ = inputs.kernel_batch(2000, 6, 5, V, 1.0, 99)
     negs = table[np.random.default_rng(98).integers(0, len(table), (2000, 5))]
