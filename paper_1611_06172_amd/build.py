@@ -17,7 +17,7 @@ LIB = os.path.join(HERE, "libw2v.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 HIP_SOURCES = ["api.hip", "epoch_kernels.hip", "pairwise_kernels.hip",
-               "step_kernels.hip", "step_sorted.hip", "vocab.hip"]
+               "step_kernels.hip", "step_sorted.hip", "vocab.hip", "radix_sort.hip"]
 CXX_SOURCES = ["tables.cpp"]
 
 HIP_FLAGS = [

@@ -129,6 +129,17 @@ hipError_t launch_vocab(const int32_t* raw, int64_t T, int32_t V,
                         int64_t min_count, int64_t* ranked_counts,
                         int32_t* rank_of, int32_t* v_kept, int32_t* corpus_out,
                         void* workspace, hipStream_t s);
+// Stable LSD radix sort of (key, value) pairs, keys < 2^bits (radix_sort.hip);
+// vals_in NULL means values 0..n-1. temp: radix_sort_temp_bytes(n,
+// sizeof(key)) bytes, 256-byte aligned; keys_out/vals_out must not overlap
+// the inputs or temp.
+size_t radix_sort_temp_bytes(int64_t n, size_t key_bytes);
+hipError_t radix_sort_pairs(const uint32_t* keys_in, const int32_t* vals_in,
+                            uint32_t* keys_out, int32_t* vals_out, int64_t n,
+                            int bits, void* temp, hipStream_t s);
+hipError_t radix_sort_pairs(const unsigned long long* keys_in, const int32_t* vals_in,
+                            unsigned long long* keys_out, int32_t* vals_out, int64_t n,
+                            int bits, void* temp, hipStream_t s);
 // Algorithm 1 (per-pair) epoch kernel.
 int pairwise_blocks_per_cu(int C, int K);
 hipError_t launch_pairwise(int C, const EpochArgs& a, int grid, hipStream_t s);

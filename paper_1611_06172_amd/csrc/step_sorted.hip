@@ -7,8 +7,8 @@
 //      (StagedRows) instead of applying them. Each staging row gets a sort
 //      key naming the matrix row it updates: id for M_in, V + id for M_out,
 //      2V for an unused staging row;
-//   2. one stable radix sort of (key, staging index) pairs (hipCUB), so each
-//      matrix row's updates form one run, in minibatch order;
+//   2. one stable radix sort of (key, staging index) pairs (radix_sort.hip),
+//      so each matrix row's updates form one run, in minibatch order;
 //   3. k_reduce: one wavefront per chunk of 64 sorted entries sums each run
 //      it holds in fp64, in sorted order, loading kBatch staging rows (and
 //      the matrix rows of the runs that open among them) at once. A run
@@ -24,7 +24,6 @@
 // Traffic per batch: the gathered rows, one staging row written and read
 // per update, the keys, and one read and write per touched row.
 #include <hip/hip_runtime.h>
-#include <hipcub/hipcub.hpp>
 
 #include "kernel_args.h"
 #include "sgns_core.h"
@@ -394,14 +393,11 @@ static int key_bits(int32_t V) {
   return 32 - __builtin_clz(2u * (unsigned)V);  // keys are 0..2V
 }
 
-// Temporary bytes of the sort of n pairs; false if the size query fails.
+// Temporary bytes of the sort of n pairs.
 static bool sort_temp_bytes(int64_t n, int32_t V, size_t& bytes) {
-  bytes = 0;
-  if (n <= 0) return true;
-  return hipcub::DeviceRadixSort::SortPairs(
-             (void*)nullptr, bytes, (const uint32_t*)nullptr, (uint32_t*)nullptr,
-             (const int32_t*)nullptr, (int32_t*)nullptr, (int)n, 0,
-             key_bits(V)) == hipSuccess;
+  (void)V;
+  bytes = radix_sort_temp_bytes(n, sizeof(uint32_t));
+  return true;
 }
 
 // Doubles per piece row: at least 64 C for the C a row stride of ld can
@@ -470,10 +466,8 @@ hipError_t launch_step_sorted(int C, int nmax, SortedStepArgs a, void* workspace
   hipLaunchKernelGGL(k, dim3(grid), dim3(kWave), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  size_t bytes = L.temp;
-  e = hipcub::DeviceRadixSort::SortPairs(temp, bytes, (const uint32_t*)keys,
-                                         keys_sorted, (const int32_t*)vals,
-                                         vals_sorted, (int)L.n, 0, key_bits(a.V), s);
+  e = radix_sort_pairs((const uint32_t*)keys, (const int32_t*)vals, keys_sorted,
+                       vals_sorted, L.n, key_bits(a.V), temp, s);
   if (e != hipSuccess) return e;
   ReduceArgs r{keys_sorted, vals_sorted, L.n, stage, a.M_in, a.M_out, pieces,
                a.V, a.D, a.ld, piece_stride((int32_t)a.ld)};

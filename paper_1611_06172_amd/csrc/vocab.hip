@@ -11,12 +11,12 @@
 //   1. histogram of the raw ids (LDS tables per workgroup, then 64-bit
 //      atomic counts; ids outside [0, V_raw) are not counted);
 //   2. a stable radix sort of the raw ids by count, descending, so equal
-//      counts keep increasing raw id order;
+//      counts keep increasing raw id order (radix_sort.hip, on the key
+//      2^b - 1 - count with b the bit length of T, ascending);
 //   3. rank r of sorted word s: new id r if its count reaches min_count,
 //      else -1; ranked counts out;
 //   4. the corpus rewritten through the rank map.
 #include <hip/hip_runtime.h>
-#include <hipcub/hipcub.hpp>
 
 #include "kernel_args.h"
 
@@ -88,26 +88,29 @@ __global__ __launch_bounds__(256) void k_vocab_zero(unsigned long long* c,
     c[i] = 0ull;
 }
 
-__global__ __launch_bounds__(256) void k_vocab_iota(int32_t* ids, int32_t V) {
+// Sort keys: top - count (top = 2^b - 1 >= every count), so that an
+// ascending sort orders the words by count, descending.
+__global__ __launch_bounds__(256) void k_vocab_keys(const unsigned long long* counts,
+                                                    int32_t V, unsigned long long top,
+                                                    unsigned long long* keys) {
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < V;
        i += (int64_t)gridDim.x * blockDim.x)
-    ids[i] = (int32_t)i;
+    keys[i] = top - counts[i];
 }
 
 __global__ __launch_bounds__(256) void k_vocab_rank(
-    const unsigned long long* sorted_counts, const int32_t* sorted_ids,
-    int32_t V, int64_t min_count, int64_t* ranked_counts, int32_t* rank_of,
-    int32_t* v_kept) {
+    const unsigned long long* sorted_keys, unsigned long long top,
+    const int32_t* sorted_ids, int32_t V, int64_t min_count, int64_t* ranked_counts,
+    int32_t* rank_of, int32_t* v_kept) {
   for (int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; r < V;
        r += (int64_t)gridDim.x * blockDim.x) {
-    const int64_t c = (int64_t)sorted_counts[r];
+    const int64_t c = (int64_t)(top - sorted_keys[r]);
     const bool keep = c >= min_count && c > 0;
     rank_of[sorted_ids[r]] = keep ? (int32_t)r : -1;
     ranked_counts[r] = keep ? c : 0;
     // counts are non-increasing in r: the last kept rank fixes the size
-    const bool next_dropped =
-        r + 1 == V || !((int64_t)sorted_counts[r + 1] >= min_count &&
-                        sorted_counts[r + 1] > 0);
+    const int64_t c_next = r + 1 < V ? (int64_t)(top - sorted_keys[r + 1]) : 0;
+    const bool next_dropped = r + 1 == V || !(c_next >= min_count && c_next > 0);
     if (keep && next_dropped) *v_kept = (int32_t)(r + 1);
     if (r == 0 && !keep) *v_kept = 0;
   }
@@ -145,22 +148,18 @@ __global__ __launch_bounds__(256) void k_vocab_remap(const int32_t* raw,
 
 static size_t align256(size_t n) { return (n + 255) / 256 * 256; }
 
-// Temporary bytes of the sort; 0 if the size query fails, in which case the
-// sort itself reports the error (its temporaries are then too small).
-static size_t sort_temp_bytes(int32_t V) {
-  size_t bytes = 0;
-  if (hipcub::DeviceRadixSort::SortPairsDescending(
-          (void*)nullptr, bytes, (const unsigned long long*)nullptr,
-          (unsigned long long*)nullptr, (const int32_t*)nullptr,
-          (int32_t*)nullptr, (int)V) != hipSuccess)
-    return 0;
-  return bytes;
+size_t vocab_workspace_bytes(int32_t V) {
+  // counts, sort keys, sorted keys, sorted ids, sort temporaries
+  return 3 * align256(sizeof(unsigned long long) * (size_t)V) +
+         align256(sizeof(int32_t) * (size_t)V) +
+         align256(radix_sort_temp_bytes(V, sizeof(unsigned long long)));
 }
 
-size_t vocab_workspace_bytes(int32_t V) {
-  // counts, sorted counts, ids, sorted ids, sort temporaries
-  return 2 * align256(sizeof(unsigned long long) * (size_t)V) +
-         2 * align256(sizeof(int32_t) * (size_t)V) + align256(sort_temp_bytes(V));
+// Bit length of T (every count is at most T), at least 1.
+static int count_bits(int64_t T) {
+  int b = 1;
+  while (b < 63 && (T >> b) != 0) ++b;
+  return b;
 }
 
 static int vocab_grid(int64_t n) {
@@ -175,28 +174,31 @@ hipError_t launch_vocab(const int32_t* raw, int64_t T, int32_t V,
   char* w = (char*)workspace;
   auto* counts = (unsigned long long*)w;
   w += align256(sizeof(unsigned long long) * (size_t)V);
-  auto* sorted_counts = (unsigned long long*)w;
+  auto* keys = (unsigned long long*)w;
   w += align256(sizeof(unsigned long long) * (size_t)V);
-  auto* ids = (int32_t*)w;
-  w += align256(sizeof(int32_t) * (size_t)V);
+  auto* sorted_keys = (unsigned long long*)w;
+  w += align256(sizeof(unsigned long long) * (size_t)V);
   auto* sorted_ids = (int32_t*)w;
   w += align256(sizeof(int32_t) * (size_t)V);
-  size_t temp_bytes = sort_temp_bytes(V);
+  const int bits = count_bits(T);
+  const unsigned long long top = (bits >= 64) ? ~0ull : ((1ull << bits) - 1ull);
 
   hipLaunchKernelGGL(k_vocab_zero, dim3(vocab_grid(V)), dim3(256), 0, s, counts, V);
   const int64_t n_chunks = (T + kChunkTokens - 1) / kChunkTokens;
   const int cgrid = (int)(n_chunks < 2048 ? (n_chunks > 0 ? n_chunks : 1) : 2048);
   hipLaunchKernelGGL(k_vocab_count, dim3(cgrid), dim3(kCountThreads), 0, s, raw, T,
                      V, counts);
-  hipLaunchKernelGGL(k_vocab_iota, dim3(vocab_grid(V)), dim3(256), 0, s, ids, V);
+  hipLaunchKernelGGL(k_vocab_keys, dim3(vocab_grid(V)), dim3(256), 0, s,
+                     (const unsigned long long*)counts, V, top, keys);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  e = hipcub::DeviceRadixSort::SortPairsDescending(
-      (void*)w, temp_bytes, (const unsigned long long*)counts, sorted_counts,
-      (const int32_t*)ids, sorted_ids, (int)V, 0, 64, s);
+  // values NULL: the raw ids 0..V-1, so equal counts keep increasing id
+  e = radix_sort_pairs((const unsigned long long*)keys, nullptr, sorted_keys, sorted_ids,
+                       (int64_t)V, bits, (void*)w, s);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_vocab_rank, dim3(vocab_grid(V)), dim3(256), 0, s,
-                     sorted_counts, sorted_ids, V, min_count, ranked_counts,
+                     (const unsigned long long*)sorted_keys, top,
+                     (const int32_t*)sorted_ids, V, min_count, ranked_counts,
                      rank_of, v_kept);
   if (corpus_out != nullptr)
     hipLaunchKernelGGL(k_vocab_remap, dim3(vocab_grid(T)), dim3(256), 0, s, raw,
