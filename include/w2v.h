@@ -179,7 +179,10 @@ int32_t w2v_pending_slots(int32_t D, int32_t window, int32_t K);
  * minibatch). Minibatches of one sentence run in order on one wavefront; up
  * to max_inflight sentences run concurrently and their updates interleave
  * without locks (Hogwild). max_inflight = 1 processes every minibatch in
- * sequence; 0 picks w2v_default_inflight(V, D, window, K, group).
+ * sequence; 0 picks min(w2v_default_inflight(V, D, window, K, group),
+ * ceil(S / 8)) for the S sentences of the range, so that they run in at
+ * least 8 rounds (with every sentence of a short range in flight at once,
+ * each would start from the initial model).
  * Pending input rows (W2V_ALGORITHM_HOGBATCH with group 1): consecutive
  * targets share most input words, so a wavefront adds the updates of a cold
  * input row (id >= max(hot_rows, split_rows)) to one of

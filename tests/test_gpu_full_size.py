@@ -78,7 +78,10 @@ def test_bench_launch_configuration_on_a_prefix():
     corpus, table, thr, M_in, hot, split = workload(10_000_000)
     s = oracle.Sampling(corpus, table, thr, window=5, K=5, seed=1234)
     mb = oracle.minibatches(s)
-    gi, go, stats, lb = run_gpu(corpus, table, thr, M_in, hot, split, max_inflight=0)
+    # the benchmark's concurrency (a default launch over only 1e4 sentences
+    # would run fewer at once, to keep 8 rounds)
+    gi, go, stats, lb = run_gpu(corpus, table, thr, M_in, hot, split,
+                                max_inflight=w2v.default_inflight(D, 5, 5, V=V))
     assert stats[0] == len(mb["targets"])
     assert stats[1] == (mb["ctx"] >= 0).sum()
     assert stats[2] == len(corpus) and stats[3] == 0
