@@ -71,6 +71,12 @@ extern "C" {
 /* Partial rows per split row of w2v_train_epoch (one per XCD of MI355X). */
 #define W2V_SPLIT_PARTS 8
 
+/* Bytes of the library's static device scratch array, the partial rows of
+ * w2v_train_epoch_noalloc (one copy per device, held until the process
+ * ends): 2 * split_rows * W2V_SPLIT_PARTS * ld * 4 bytes must fit, e.g.
+ * 204 split rows at ld = 320. */
+#define W2V_NOALLOC_SCRATCH_BYTES 4194304
+
 /* The `algorithm` argument of w2v_train_epoch. */
 #define W2V_ALGORITHM_HOGBATCH 0  /* Sec. 1.1: minibatch, shared negatives */
 #define W2V_ALGORITHM_PAIRWISE 1  /* Alg. 1: per-pair SGD, private negatives */
@@ -85,8 +91,11 @@ const char* w2v_last_error(void);
 
 /* Sets up the library's per-device state on the current HIP device: the
  * device's error word (pinned host memory mapped into the device, 256 bytes,
- * held until the process ends). Every GPU entry point does this itself on its
- * first call on a device. Safe to call repeatedly and from several threads. */
+ * held until the process ends) and the device address of the library's
+ * static scratch array. Every GPU entry point does this itself on its first
+ * call on a device, except w2v_train_epoch_noalloc, which allocates nothing
+ * and so needs w2v_init to have run on the device first. Safe to call
+ * repeatedly and from several threads. */
 int w2v_init(void);
 
 /* Waits for `stream` (a hipStream_t; NULL is the null stream), then returns
@@ -271,6 +280,33 @@ int w2v_train_epoch(const int32_t* corpus, int64_t T, int64_t pos_begin,
                     int32_t hot_rows, int32_t split_rows, void* workspace,
                     size_t workspace_bytes, int32_t algorithm, int32_t group,
                     void* stream);
+
+/*
+ * w2v_train_epoch for callers that cannot allocate (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * arguments, readings, limits and results, minus the workspace. The split
+ * rows' partial rows live in the library's static device scratch array
+ * (W2V_NOALLOC_SCRATCH_BYTES per device), so split_rows must satisfy
+ * 2 * split_rows * W2V_SPLIT_PARTS * ld * 4 <= W2V_NOALLOC_SCRATCH_BYTES,
+ * else W2V_EINVAL (nothing launched). The call allocates no device or
+ * pinned memory and calls no hipMalloc or hipFree; w2v_init must have run
+ * on the current device (else W2V_EINVAL). It clears the partial rows it
+ * uses before the epoch (with a kernel, no memset) and after it. All calls
+ * on one device share the one scratch array: calls that overlap in time on
+ * the same device (other streams, other threads) race on it and must not
+ * be issued. (A shape's launch configuration is computed on its first call
+ * and cached in host memory.)
+ */
+int w2v_train_epoch_noalloc(const int32_t* corpus, int64_t T, int64_t pos_begin,
+                            int64_t pos_end, int32_t sentence_len, float* M_in,
+                            float* M_out, int32_t V, int32_t D, int32_t ld,
+                            int32_t window, int32_t K, const int32_t* neg_table,
+                            int64_t table_size, const uint32_t* keep_thresh,
+                            float alpha0, float min_alpha_frac, int32_t epoch,
+                            int32_t n_epochs, uint64_t seed, double* loss_buckets,
+                            int32_t n_buckets, int64_t* stats, int32_t max_inflight,
+                            int32_t hot_rows, int32_t split_rows, int32_t algorithm,
+                            int32_t group, void* stream);
 
 /* Workspace bytes w2v_train_epoch needs for split_rows rows of stride ld:
  * 2 * split_rows * W2V_SPLIT_PARTS * ld * 4 (0 when split_rows is 0). */

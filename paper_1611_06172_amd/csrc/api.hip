@@ -49,6 +49,7 @@ struct DeviceState {
   bool ready = false;
   volatile int32_t* status_host = nullptr;  // what the host reads
   int32_t* status_dev = nullptr;            // the same word, device address
+  void* scratch = nullptr;                  // this device's copy of `scratch`
 };
 
 static std::mutex g_dev_mu;
@@ -62,10 +63,22 @@ static int current_device(int& dev) {
   return W2V_OK;
 }
 
+// Scratch memory of w2v_train_epoch_noalloc: the split rows' partial rows,
+// W2V_NOALLOC_SCRATCH_BYTES per device, held until the process ends. Host
+// code never passes `scratch` itself to a kernel (in host code it names a
+// host-side stand-in); it uses the device address hipGetSymbolAddress gives
+// for the current device, recorded in DeviceState::scratch.
+static __device__ __align__(256) unsigned char scratch[W2V_NOALLOC_SCRATCH_BYTES];
+
 // Sets up the current device's state once (caller holds g_dev_mu).
 static int setup_device_locked(int dev) {
   DeviceState& st = g_dev[dev];
   if (st.ready) return W2V_OK;
+  void* sym = nullptr;
+  hipError_t es = hipGetSymbolAddress(&sym, HIP_SYMBOL(scratch));
+  if (es != hipSuccess) return hip_fail(es, "hipGetSymbolAddress of the scratch array");
+  if (sym == nullptr || ((uintptr_t)sym & 255u) != 0)
+    return fail(W2V_EHIP, "scratch array address is NULL or not 256-byte aligned");
   void* host = nullptr;
   hipError_t e = hipHostMalloc(&host, 256, hipHostMallocMapped | hipHostMallocCoherent);
   if (e != hipSuccess) return hip_fail(e, "hipHostMalloc of the error word");
@@ -78,21 +91,32 @@ static int setup_device_locked(int dev) {
   st.status_host = (volatile int32_t*)host;
   *st.status_host = 0;
   st.status_dev = (int32_t*)mapped;
+  st.scratch = sym;
   st.ready = true;
   return W2V_OK;
 }
 
-// Entry check of every GPU call: sets up the device if needed, reports (and
-// clears) a skip recorded by an earlier call, and gives the kernels the
-// error word. A reported skip means this call launched nothing.
-static int enter_device(int32_t** status_dev) {
+// Entry check of every GPU call: sets up the device if needed (unless
+// `no_setup`, for the entry point that must not allocate: it then fails
+// when w2v_init has not run on the device), reports (and clears) a skip
+// recorded by an earlier call, and gives the kernels the error word and
+// the device's scratch address. A reported skip means this call launched
+// nothing.
+static int enter_device(int32_t** status_dev, void** scratch_dev = nullptr,
+                        bool no_setup = false) {
   int dev = 0;
   int rc = current_device(dev);
   if (rc != W2V_OK) return rc;
   std::lock_guard<std::mutex> lock(g_dev_mu);
+  if (no_setup && !g_dev[dev].ready)
+    return failf(W2V_EINVAL,
+                 "w2v_init has not run on device %d: the entry point that allocates "
+                 "nothing needs it first",
+                 dev);
   rc = setup_device_locked(dev);
   if (rc != W2V_OK) return rc;
   DeviceState& st = g_dev[dev];
+  if (scratch_dev != nullptr) *scratch_dev = st.scratch;
   if (*st.status_host != 0) {
     *st.status_host = 0;
     return failf(W2V_EDEVICE_FLAG,
@@ -291,17 +315,23 @@ int32_t w2v_pending_slots(int32_t D, int32_t window, int32_t K) {
   return train_pending_slots(C, nmax, K);
 }
 
-int w2v_train_epoch(const int32_t* corpus, int64_t T, int64_t pos_begin,
-                    int64_t pos_end, int32_t sentence_len, float* M_in,
-                    float* M_out, int32_t V, int32_t D, int32_t ld,
-                    int32_t window, int32_t K, const int32_t* neg_table,
-                    int64_t table_size, const uint32_t* keep_thresh,
-                    float alpha0, float min_alpha_frac, int32_t epoch,
-                    int32_t n_epochs, uint64_t seed, double* loss_buckets,
-                    int32_t n_buckets, int64_t* stats, int32_t max_inflight,
-                    int32_t hot_rows, int32_t split_rows, void* workspace,
-                    size_t workspace_bytes, int32_t algorithm, int32_t group,
-                    void* stream) {
+}  // extern "C"
+
+namespace w2v {
+
+// w2v_train_epoch and w2v_train_epoch_noalloc: with `noalloc` the partial
+// rows live in the device's scratch array instead of the caller's workspace.
+static int train_epoch_impl(const int32_t* corpus, int64_t T, int64_t pos_begin,
+                            int64_t pos_end, int32_t sentence_len, float* M_in,
+                            float* M_out, int32_t V, int32_t D, int32_t ld,
+                            int32_t window, int32_t K, const int32_t* neg_table,
+                            int64_t table_size, const uint32_t* keep_thresh,
+                            float alpha0, float min_alpha_frac, int32_t epoch,
+                            int32_t n_epochs, uint64_t seed, double* loss_buckets,
+                            int32_t n_buckets, int64_t* stats, int32_t max_inflight,
+                            int32_t hot_rows, int32_t split_rows, void* workspace,
+                            size_t workspace_bytes, int32_t algorithm, int32_t group,
+                            void* stream, bool noalloc) {
   int rc = check_sampling({corpus, T, pos_begin, pos_end, sentence_len, V,
                            window, K, neg_table, table_size, epoch, n_epochs});
   if (rc != W2V_OK) return rc;
@@ -328,7 +358,13 @@ int w2v_train_epoch(const int32_t* corpus, int64_t T, int64_t pos_begin,
     return fail(W2V_EINVAL,
                 "group needs 2 window group <= 64, 2 window + group <= 32 and "
                 "group + K <= 32");
-  if (split_rows > 0) {
+  if (noalloc && w2v_train_epoch_workspace_bytes(split_rows, ld) > W2V_NOALLOC_SCRATCH_BYTES)
+    return failf(W2V_EINVAL,
+                 "split_rows = %d at ld = %d needs %zu bytes of partial rows, more than "
+                 "the %d bytes of scratch of w2v_train_epoch_noalloc",
+                 split_rows, ld, w2v_train_epoch_workspace_bytes(split_rows, ld),
+                 W2V_NOALLOC_SCRATCH_BYTES);
+  if (split_rows > 0 && !noalloc) {
     if (workspace == nullptr) return fail(W2V_EINVAL, "workspace is NULL");
     if (workspace_bytes < w2v_train_epoch_workspace_bytes(split_rows, ld))
       return fail(W2V_EINVAL, "workspace too small for split_rows");
@@ -350,8 +386,10 @@ int w2v_train_epoch(const int32_t* corpus, int64_t T, int64_t pos_begin,
     return failf(W2V_EUNSUPPORTED, "no compiled kernel for D=%d window=%d", D,
                  window);
   int32_t* status = nullptr;
-  rc = enter_device(&status);
+  void* scratch_dev = nullptr;
+  rc = enter_device(&status, &scratch_dev, noalloc);
   if (rc != W2V_OK) return rc;
+  if (noalloc) workspace = scratch_dev;
   const int64_t n_sent = (pos_end - pos_begin + sentence_len - 1) / sentence_len;
   if (n_sent == 0) return ok();
 
@@ -420,6 +458,45 @@ int w2v_train_epoch(const int32_t* corpus, int64_t T, int64_t pos_begin,
     if (e != hipSuccess) return hip_fail(e, "partial-row fold launch");
   }
   return ok();
+}
+
+}  // namespace w2v
+
+extern "C" {
+
+int w2v_train_epoch(const int32_t* corpus, int64_t T, int64_t pos_begin,
+                    int64_t pos_end, int32_t sentence_len, float* M_in,
+                    float* M_out, int32_t V, int32_t D, int32_t ld,
+                    int32_t window, int32_t K, const int32_t* neg_table,
+                    int64_t table_size, const uint32_t* keep_thresh,
+                    float alpha0, float min_alpha_frac, int32_t epoch,
+                    int32_t n_epochs, uint64_t seed, double* loss_buckets,
+                    int32_t n_buckets, int64_t* stats, int32_t max_inflight,
+                    int32_t hot_rows, int32_t split_rows, void* workspace,
+                    size_t workspace_bytes, int32_t algorithm, int32_t group,
+                    void* stream) {
+  return train_epoch_impl(corpus, T, pos_begin, pos_end, sentence_len, M_in, M_out, V,
+                          D, ld, window, K, neg_table, table_size, keep_thresh, alpha0,
+                          min_alpha_frac, epoch, n_epochs, seed, loss_buckets, n_buckets,
+                          stats, max_inflight, hot_rows, split_rows, workspace,
+                          workspace_bytes, algorithm, group, stream, false);
+}
+
+int w2v_train_epoch_noalloc(const int32_t* corpus, int64_t T, int64_t pos_begin,
+                            int64_t pos_end, int32_t sentence_len, float* M_in,
+                            float* M_out, int32_t V, int32_t D, int32_t ld,
+                            int32_t window, int32_t K, const int32_t* neg_table,
+                            int64_t table_size, const uint32_t* keep_thresh,
+                            float alpha0, float min_alpha_frac, int32_t epoch,
+                            int32_t n_epochs, uint64_t seed, double* loss_buckets,
+                            int32_t n_buckets, int64_t* stats, int32_t max_inflight,
+                            int32_t hot_rows, int32_t split_rows, int32_t algorithm,
+                            int32_t group, void* stream) {
+  return train_epoch_impl(corpus, T, pos_begin, pos_end, sentence_len, M_in, M_out, V,
+                          D, ld, window, K, neg_table, table_size, keep_thresh, alpha0,
+                          min_alpha_frac, epoch, n_epochs, seed, loss_buckets, n_buckets,
+                          stats, max_inflight, hot_rows, split_rows, nullptr, 0,
+                          algorithm, group, stream, true);
 }
 
 size_t w2v_train_epoch_workspace_bytes(int32_t split_rows, int32_t ld) {

@@ -63,6 +63,9 @@ def lib():
         _vp, _i64, _vp, _f32, _f32, _i32, _i32, _u64, _vp, _i32, _vp, _i32, _i32,
         _i32, _vp, ctypes.c_size_t, _i32, _i32, _vp]
     L.w2v_train_epoch.restype = ctypes.c_int
+    L.w2v_train_epoch_noalloc.argtypes = (L.w2v_train_epoch.argtypes[:26] +
+                                          L.w2v_train_epoch.argtypes[28:])
+    L.w2v_train_epoch_noalloc.restype = ctypes.c_int
     L.w2v_build_vocab_workspace_bytes.argtypes = [_i32]
     L.w2v_build_vocab_workspace_bytes.restype = ctypes.c_size_t
     L.w2v_build_vocab.argtypes = [_vp, _i64, _i32, _i64, _vp, _vp, _vp, _vp, _vp,
@@ -271,6 +274,51 @@ def train_epoch(corpus, M_in, M_out, neg_table, keep_thresh=None, *,
         V if hot_rows is None else int(hot_rows), int(split_rows),
         _ptr(workspace), ws_bytes, ALGORITHMS[algorithm], int(group),
         _stream(stream)))
+
+
+NOALLOC_SCRATCH_BYTES = 4194304
+
+
+def train_epoch_noalloc(corpus, M_in, M_out, neg_table, keep_thresh=None, *,
+                        window: int = 5, K: int = 5, D: Optional[int] = None,
+                        alpha0: float = 0.025, min_alpha_frac: float = 1e-4,
+                        epoch: int = 0, n_epochs: int = 1, seed: int = 0,
+                        pos_begin: int = 0, pos_end: Optional[int] = None,
+                        sentence_len: int = 1000, loss_buckets=None, stats=None,
+                        max_inflight: int = 0, hot_rows: Optional[int] = None,
+                        split_rows: int = 0, algorithm: str = "hogbatch",
+                        group: int = 1, stream=None):
+    """train_epoch through w2v_train_epoch_noalloc: the split rows' partial
+    rows live in the library's static device scratch array, so nothing is
+    allocated here or in the library. init() must have run on the device."""
+    import torch
+    _dev(corpus, torch.int32, "corpus", 1)
+    V, ld = _matrix(M_in, "M_in")
+    if _matrix(M_out, "M_out") != (V, ld):
+        raise ValueError("M_in and M_out must have the same shape and stride")
+    D = M_in.shape[1] if D is None else D
+    _dev(neg_table, torch.int32, "neg_table", 1)
+    if keep_thresh is not None:
+        _dev(keep_thresh, (torch.int32, torch.uint32), "keep_thresh", 1)
+        if keep_thresh.numel() != V:
+            raise ValueError("keep_thresh must have V entries")
+    n_b = 0
+    if loss_buckets is not None:
+        _dev(loss_buckets, torch.float64, "loss_buckets", 2)
+        n_b = loss_buckets.shape[0]
+    if stats is not None:
+        _dev(stats, torch.int64, "stats", 1)
+        if stats.numel() < 5:
+            raise ValueError("stats must have 5 entries (see w2v_train_epoch)")
+    T = corpus.numel()
+    end = T if pos_end is None else pos_end
+    _check(lib().w2v_train_epoch_noalloc(
+        _ptr(corpus), T, pos_begin, end, sentence_len, _ptr(M_in), _ptr(M_out),
+        V, D, ld, window, K, _ptr(neg_table), neg_table.numel(),
+        _ptr(keep_thresh), alpha0, min_alpha_frac, epoch, n_epochs, seed,
+        _ptr(loss_buckets), n_b, _ptr(stats), max_inflight,
+        V if hot_rows is None else int(hot_rows), int(split_rows),
+        ALGORITHMS[algorithm], int(group), _stream(stream)))
 
 
 def padded_ld(D: int) -> int:
