@@ -129,12 +129,13 @@ def main():
                          "(hogbatch_immediate) run after the headline, reported "
                          "beside it (0: skip)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--workload", choices=["large-vocab", "kernel-test", "vocab"],
+    ap.add_argument("--workload", choices=["large-vocab", "kernel-test", "vocab", "row-rmw"],
                     default="large-vocab",
                     help="large-vocab: the HogBatch epoch (the measured path); "
                          "kernel-test: one snapshot batch of 65,536 minibatches "
                          "(w2v_step_batch); vocab: the vocabulary pipeline "
-                         "(w2v_build_vocab) over --tokens raw ids")
+                         "(w2v_build_vocab) over --tokens raw ids; row-rmw: the memory "
+                         "system's rate for the epoch's row accesses (measurement kernel)")
     ap.add_argument("--step-mode", choices=["sorted", "atomic"], default="sorted",
                     help="kernel-test: w2v_step_batch_sorted or w2v_step_batch")
     ap.add_argument("--traffic-json",
@@ -151,6 +152,9 @@ def main():
         return
     if args.workload == "vocab":
         vocab_bench(args)
+        return
+    if args.workload == "row-rmw":
+        row_rmw_bench(args)
         return
 
     import numpy as np
@@ -536,6 +540,97 @@ def vocab_bench(args):
                        f"pinned to CPU {cpu}, {c_dt:.1f}s; CPU {cpu_model()}, "
                        f"{n_cpu} CPUs available to the process"),
         }
+    print(json.dumps(result), flush=True)
+
+
+def row_rmw_bench(args):
+    """The memory system's rate for the epoch's row accesses, without the
+    method: the rows of the first 2e7 tokens' minibatches (the throughput
+    workload's sampling, exported by w2v_debug_minibatches: input rows, the
+    target and the negatives, in minibatch order), taken 12 per step by 2048
+    wavefronts as the epoch's 2048 sentences in flight take them, each row
+    read and written back in place (coherent load, write-through store) or,
+    for the last `atomic_rows` of a step, added with fp32 atomics. Rows of
+    D = 300 floats at ld = 320 in a 1e6-row matrix. Also uniform random ids.
+    Bytes are counted as the epoch's algorithmic bytes: every row read and
+    written once (2 x 1200 B)."""
+    import ctypes
+    import numpy as np
+    import torch
+
+    from paper_1611_06172_amd import inputs, w2v
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    V, D, W, K, T = 1_000_000, 300, 5, 5, 20_000_000
+    corpus = inputs.zipf_corpus_hashed(T, V, 1.07, 6, dev)
+    counts = torch.bincount(corpus, minlength=V).cpu().numpy().astype(np.int64)
+    table_h, thr_h = w2v.build_tables(counts, 0.75, 1e-4, 10**8)
+    table = torch.from_numpy(table_h).to(dev)
+    thr = torch.from_numpy(thr_h.view(np.int32)).to(dev)
+    mb = w2v.debug_minibatches(corpus, table, thr, V=V, window=W, K=K, seed=1234)
+    keep = mb["targets"] >= 0
+    R = torch.cat([mb["ctx"][keep], mb["targets"][keep][:, None], mb["negs"][keep]], 1)
+    R = R.reshape(-1)
+    R = R[R >= 0]
+    rows = 12
+    n_steps = R.numel() // rows
+    epoch_ids = R[: n_steps * rows].contiguous()
+    g = torch.Generator(device=dev)
+    g.manual_seed(12)
+    uniform_ids = torch.randint(0, V, (n_steps * rows,), generator=g, device=dev,
+                                dtype=torch.int32)
+    del corpus, mb, R
+    M = w2v.alloc_matrix(V, D, dev)
+    ld = M.stride(0)
+    L = ctypes.CDLL(os.path.join(ROOT, "paper_1611_06172_amd", "libw2v_measure.so"))
+    L.w2v_measure_row_rmw.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32,
+                                      ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64,
+                                      ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                                      ctypes.c_void_p]
+    stream = torch.cuda.current_stream()
+    grid = args.max_inflight or 2048
+    results = {}
+    for label, ids, n_atomic in (("epoch rows, 3 of 12 atomic", epoch_ids, 3),
+                                 ("epoch rows, no atomics", epoch_ids, 0),
+                                 ("uniform rows, no atomics", uniform_ids, 0)):
+        def call():
+            rc = L.w2v_measure_row_rmw(M.data_ptr(), V, D, ld, ids.data_ptr(), n_steps,
+                                       rows, n_atomic, grid, stream.cuda_stream)
+            if rc != 0:
+                raise RuntimeError(f"w2v_measure_row_rmw failed ({rc})")
+        for _ in range(max(args.warmup, 1)):
+            call()
+        steps = max(args.steps, 1)
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(steps)]
+        torch.cuda.synchronize()
+        for i in range(steps):
+            evs[i][0].record(stream)
+            call()
+            evs[i][1].record(stream)
+        torch.cuda.synchronize()
+        ms = float(np.mean([a.elapsed_time(b) for a, b in evs]))
+        gbs = 2.0 * 4 * D * n_steps * rows / (ms * 1e-3) / 1e9
+        results[label] = {"ms": round(ms, 3), "GBs": round(gbs, 1)}
+        print(f"[bench] row-rmw {label}: {ms:.2f} ms, {gbs:.0f} GB/s", file=sys.stderr,
+              flush=True)
+    head = results["epoch rows, 3 of 12 atomic"]
+    result = {
+        "metric": "GB/s, random row read-modify-write (the epoch's row accesses without "
+                  "the method)",
+        "value": head["GBs"], "unit": "GB/s", "n_gpus": 1, "steps": max(args.steps, 1),
+        "warmup": max(args.warmup, 1), "ms_per_step": head["ms"],
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": f"rows of the throughput workload's first {T} tokens' "
+                               f"minibatches, {rows} per step, {grid} wavefronts, D={D}, "
+                               f"ld={ld}, V={V}",
+                   "steps_per_call": n_steps, "rows_per_step": rows, "variants": results},
+        "roofline": {"bound": "hbm", "kernel": "k_row_rmw", "achieved": head["GBs"],
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(head["GBs"] / HBM_PEAK_GBS, 4), "traffic": None},
+    }
     print(json.dumps(result), flush=True)
 
 
