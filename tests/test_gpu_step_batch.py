@@ -134,3 +134,30 @@ def test_empty_batch_and_validation():
         ws = torch.empty(16, dtype=torch.uint8, device="cuda")
         t = torch.zeros(2, dtype=torch.int32, device="cuda")
         w2v.step_batch(t, t.view(2, 1), t.view(2, 1), M, M.clone(), workspace=ws)
+
+
+def test_strided_views_are_rejected():
+    """The kernels read contexts, negatives and loss buckets as packed
+    arrays; a strided view would be read at the wrong places, so the
+    binding refuses it (the row-padded matrices, whose stride is passed as
+    ld, are the only strided arguments)."""
+    import torch
+    V, D = 50, 16
+    M_in = torch.zeros((V, D), device="cuda")
+    M_out = torch.zeros((V, D), device="cuda")
+    t = torch.zeros(8, dtype=torch.int32, device="cuda")
+    wide = torch.zeros((8, 12), dtype=torch.int32, device="cuda")
+    negs = torch.zeros((8, 3), dtype=torch.int32, device="cuda")
+    with pytest.raises(ValueError):
+        w2v.step_batch(t, wide[:, :10], negs, M_in, M_out)
+    with pytest.raises(ValueError):
+        w2v.step_batch(t, wide[:, :4].contiguous(), wide[:, ::4], M_in, M_out)
+    c = torch.zeros(3000, dtype=torch.int32, device="cuda")
+    tb = torch.zeros(10, dtype=torch.int32, device="cuda")
+    lb = torch.zeros((4, 3), dtype=torch.float64, device="cuda")[:, :2]
+    with pytest.raises(ValueError):
+        w2v.train_epoch(c, M_in, M_out, tb, loss_buckets=lb)
+    # a padded matrix view is accepted
+    P = w2v.alloc_matrix(V, D, "cuda")
+    assert P.stride(0) == 32
+    w2v.step_batch(t, wide[:, :4].contiguous(), negs, P, w2v.alloc_matrix(V, D, "cuda"))
