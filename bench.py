@@ -480,7 +480,7 @@ def vocab_bench(args):
     rank_of = torch.empty(V_raw, dtype=torch.int32, device=dev)
     v_kept = torch.empty(1, dtype=torch.int32, device=dev)
     corpus = torch.empty(T, dtype=torch.int32, device=dev)
-    ws = torch.empty(int(L.w2v_build_vocab_workspace_bytes(V_raw)), dtype=torch.uint8,
+    ws = torch.empty(int(L.w2v_build_vocab_workspace_bytes(V_raw, T)), dtype=torch.uint8,
                      device=dev)
     stream = torch.cuda.current_stream()
 

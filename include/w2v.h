@@ -328,10 +328,12 @@ size_t w2v_train_epoch_workspace_bytes(int32_t split_rows, int32_t ld);
  *                 such positions before forming windows).
  * With ids ranked this way id 0 is the most frequent word, as the update
  * tiers of w2v_train_epoch assume. workspace: device, 256-byte aligned,
- * >= w2v_build_vocab_workspace_bytes(V_raw) bytes, caller-owned. The call
- * is asynchronous on `stream`.
+ * >= w2v_build_vocab_workspace_bytes(V_raw, T) bytes, caller-owned; up to
+ * V_raw = 4,194,304 the ids are counted by id range without atomics to
+ * device memory, which takes about 4.3 T bytes of it (the stream reordered
+ * by id range, and partial counts). The call is asynchronous on `stream`.
  */
-size_t w2v_build_vocab_workspace_bytes(int32_t V_raw);
+size_t w2v_build_vocab_workspace_bytes(int32_t V_raw, int64_t T);
 int w2v_build_vocab(const int32_t* raw, int64_t T, int32_t V_raw,
                     int64_t min_count, int64_t* ranked_counts,
                     int32_t* rank_of, int32_t* v_kept, int32_t* corpus_out,

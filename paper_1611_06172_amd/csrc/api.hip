@@ -238,7 +238,7 @@ using namespace w2v;
 
 extern "C" {
 
-int w2v_version(void) { return 101; }
+int w2v_version(void) { return 102; }
 
 const char* w2v_last_error(void) { return g_error; }
 
@@ -685,9 +685,9 @@ int w2v_step_batch_sorted(int32_t B, int32_t N, int32_t K, const int32_t* target
   return ok();
 }
 
-size_t w2v_build_vocab_workspace_bytes(int32_t V_raw) {
-  if (V_raw <= 0) return 0;
-  return vocab_workspace_bytes(V_raw);
+size_t w2v_build_vocab_workspace_bytes(int32_t V_raw, int64_t T) {
+  if (V_raw <= 0 || T < 0) return 0;
+  return vocab_workspace_bytes(V_raw, T);
 }
 
 int w2v_build_vocab(const int32_t* raw, int64_t T, int32_t V_raw,
@@ -700,9 +700,9 @@ int w2v_build_vocab(const int32_t* raw, int64_t T, int32_t V_raw,
   if (min_count < 0) return fail(W2V_EINVAL, "min_count must be >= 0");
   if (ranked_counts == nullptr || rank_of == nullptr || v_kept == nullptr)
     return fail(W2V_EINVAL, "ranked_counts, rank_of and v_kept must not be NULL");
-  if (workspace == nullptr || workspace_bytes < w2v_build_vocab_workspace_bytes(V_raw))
+  if (workspace == nullptr || workspace_bytes < w2v_build_vocab_workspace_bytes(V_raw, T))
     return failf(W2V_EINVAL, "workspace must hold %zu bytes",
-                 w2v_build_vocab_workspace_bytes(V_raw));
+                 w2v_build_vocab_workspace_bytes(V_raw, T));
   if (((uintptr_t)workspace & 255u) != 0)
     return fail(W2V_EINVAL, "workspace must be 256-byte aligned");
   int32_t* status = nullptr;

@@ -66,7 +66,7 @@ def lib():
     L.w2v_train_epoch_noalloc.argtypes = (L.w2v_train_epoch.argtypes[:26] +
                                           L.w2v_train_epoch.argtypes[28:])
     L.w2v_train_epoch_noalloc.restype = ctypes.c_int
-    L.w2v_build_vocab_workspace_bytes.argtypes = [_i32]
+    L.w2v_build_vocab_workspace_bytes.argtypes = [_i32, _i64]
     L.w2v_build_vocab_workspace_bytes.restype = ctypes.c_size_t
     L.w2v_build_vocab.argtypes = [_vp, _i64, _i32, _i64, _vp, _vp, _vp, _vp, _vp,
                                   ctypes.c_size_t, _vp]
@@ -455,7 +455,7 @@ def build_vocab(raw, V_raw: int, min_count: int = 0, remap: bool = True,
     rank_of = torch.empty(V_raw, dtype=torch.int32, device=dev)
     v_kept = torch.empty(1, dtype=torch.int32, device=dev)
     corpus = torch.empty(T, dtype=torch.int32, device=dev) if remap else None
-    ws = torch.empty(int(lib().w2v_build_vocab_workspace_bytes(V_raw)),
+    ws = torch.empty(int(lib().w2v_build_vocab_workspace_bytes(V_raw, T)),
                      dtype=torch.uint8, device=dev)
     _check(lib().w2v_build_vocab(_ptr(raw), T, V_raw, int(min_count), _ptr(ranked),
                                  _ptr(rank_of), _ptr(v_kept), _ptr(corpus), _ptr(ws),

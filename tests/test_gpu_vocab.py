@@ -14,6 +14,9 @@ pytestmark = pytest.mark.gpu
 @pytest.mark.parametrize("V_raw,T,min_count", [
     (8, 16, 2), (50_000, 1_000_000, 3), (1000, 0, 0), (300, 5000, 10_000), (1, 10, 0),
     (200_000, 5_000_001, 5),   # several 2^20-token chunks; tables overflow
+    (30_000, 5_000_000, 0),    # one id range (bin) cut into several count units
+    (4_194_304, 3_000_000, 1), # the largest vocabulary counted by bins: 128 bins
+    (4_194_305, 1_000_000, 1), # one id more: the hash-table count
 ])
 def test_vocab_matches_reference(V_raw, T, min_count):
     import torch

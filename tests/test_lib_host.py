@@ -30,7 +30,7 @@ def test_exports_every_declared_symbol():
 
 
 def test_version():
-    assert w2v.version() == 101
+    assert w2v.version() == 102
 
 
 @pytest.mark.parametrize("seed,power,t,size", [
@@ -173,6 +173,18 @@ def vocab(**over):
 def test_build_vocab_rejects(over, needle):
     assert vocab(**over) == w2v.EINVAL
     assert needle in w2v.lib().w2v_last_error().decode()
+
+
+def test_build_vocab_workspace_sizes():
+    """Up to 4,194,304 raw ids the ids are counted by bins, whose workspace
+    holds the binned corpus (at least 4 bytes per token); above, the count
+    needs no T-sized workspace."""
+    ws = w2v.lib().w2v_build_vocab_workspace_bytes
+    assert ws(0, 10) == 0 and ws(10, -1) == 0
+    for V in (1, 32768, 32769, 2_000_000, 4_194_304):
+        assert ws(V, 10**6) - ws(V, 0) >= 4 * 10**6
+        assert ws(V, 10**7) - ws(V, 10**6) >= 4 * 9 * 10**6
+    assert ws(4_194_305, 10**7) == ws(4_194_305, 0)
 
 
 @pytest.mark.parametrize("args,needle", [
