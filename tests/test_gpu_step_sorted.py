@@ -54,6 +54,7 @@ def test_kernel_test_config_full_size_and_reproducible():
     (900, 200, 200, 1000, 16, 25),
     (600, 100, 100, 800, 32, 64),
     (50, 96, 96, 400, 6, 0),
+    (6, 300, 320, 2000, 10, 5),    # six rows: every run crosses many chunks
 ])
 def test_shapes(V, D, ld, B, N, K):
     print(f"[sorted] V={V} D={D} ld={ld} B={B} N={N} K={K}", flush=True)
@@ -73,13 +74,15 @@ def test_absent_inputs_masks_and_per_minibatch_alpha():
     check(t, c, n, *mats(V, D, 9), alpha, sorted=True)
 
 
-def test_rows_shared_by_every_minibatch():
+@pytest.mark.parametrize("shared", [(3, 1, 2, 2, 5, 0), (40, 41, 42, 42, 45, 8)])
+def test_rows_shared_by_every_minibatch(shared):
     """Every minibatch has the same target and negatives: their runs span
-    every chunk of the output sort, and the head rows of the inputs most."""
+    every chunk of the output sort, and the head rows of the inputs most
+    (the head ids of a Zipf law, then ids from the middle of the range)."""
     V, D, B = 64, 300, 4096
-    t = np.full(B, 3, np.int32)
+    t = np.full(B, shared[0], np.int32)
     c = inputs.zipf_ids((B, 10), V, 0.5, 5)
-    n = np.tile(np.array([[1, 2, 2, 5, 0]], np.int32), (B, 1))
+    n = np.tile(np.array([shared[1:]], np.int32), (B, 1))
     check(t, c, n, *mats(V, D, 11), 0.001, sorted=True)
 
 
