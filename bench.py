@@ -143,8 +143,8 @@ def main():
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path "
-              "(see the sharding design); run with --gpus 1", file=sys.stderr)
+        print("bench.py measures one GPU only: the library has no multi-GPU path "
+              "(sharding is a design, not code); run with --gpus 1", file=sys.stderr)
         sys.exit(2)
 
     if args.workload == "kernel-test":
@@ -285,6 +285,10 @@ def main():
             "split_rows": int(split),
             "minibatches_per_step": int(n_mb), "mean_inputs_per_minibatch":
                 round(sum_n / max(n_mb, 1), 4), "retained_fraction": round(n_mb / raw, 4),
+            "steps_are": (f"epochs {args.warmup}..{args.warmup + args.steps - 1} of a "
+                          f"{n_epochs}-epoch schedule (alpha decays over the schedule; each "
+                          f"epoch continues from the previous one's matrices), after "
+                          f"{args.warmup} untimed"),
         },
         "roofline": {
             "bound": "hbm",
