@@ -56,6 +56,7 @@ extern "C" {
 #define W2V_EUNSUPPORTED (-4)/* valid arguments outside the compiled shapes */
 #define W2V_EDEVICE_FLAG (-5)/* an earlier call skipped work for an id outside
                                 [0, V); nothing was launched by this call */
+#define W2V_ENONFINITE (-6)  /* a loss bucket holds NaN or Inf (w2v_check_loss) */
 
 /* Shape limits of the compiled kernels. The HogBatch kernels keep all N
  * input rows of a minibatch in registers, so they compile D <= 640 for up to
@@ -103,6 +104,17 @@ int w2v_init(void);
  * the current device skipped a minibatch for an id outside [0, V) since the
  * word was last reported, else W2V_OK. */
 int w2v_device_status(void* stream);
+
+/* Failure detection for training (not in the paper, which reports no loss):
+ * waits for `stream`, reads the n_buckets (sum, count) pairs of
+ * loss_buckets (device double[n_buckets][2], as w2v_train_epoch fills them)
+ * and returns W2V_ENONFINITE, naming the first such bucket, if a sum or a
+ * count is NaN or Inf; W2V_OK otherwise. A NaN or Inf that reaches a row of
+ * M_in or M_out makes the loss of every later minibatch reading the row
+ * non-finite, so its bucket flags it. Launches nothing; copies 16 n_buckets
+ * bytes to the host. W2V_EINVAL for n_buckets < 0 or a NULL pointer with
+ * n_buckets > 0. */
+int w2v_check_loss(const double* loss_buckets, int32_t n_buckets, void* stream);
 
 /*
  * Sampling tables from unigram counts (host only; no HIP call).

@@ -238,7 +238,7 @@ using namespace w2v;
 
 extern "C" {
 
-int w2v_version(void) { return 102; }
+int w2v_version(void) { return 103; }
 
 const char* w2v_last_error(void) { return g_error; }
 
@@ -257,6 +257,35 @@ int w2v_device_status(void* stream) {
   int32_t* unused = nullptr;
   const int rc = enter_device(&unused);
   return rc == W2V_OK ? ok() : rc;
+}
+
+int w2v_check_loss(const double* loss_buckets, int32_t n_buckets, void* stream) {
+  if (n_buckets < 0) return fail(W2V_EINVAL, "n_buckets must be >= 0");
+  if (n_buckets > 0 && loss_buckets == nullptr)
+    return fail(W2V_EINVAL, "loss_buckets is NULL");
+  if (n_buckets == 0) return ok();
+  const size_t bytes = sizeof(double) * 2 * (size_t)n_buckets;
+  double* h = (double*)malloc(bytes);
+  if (h == nullptr) return fail(W2V_ENOMEM, "host copy of the loss buckets");
+  hipError_t e = hipMemcpyAsync(h, loss_buckets, bytes, hipMemcpyDeviceToHost,
+                                (hipStream_t)stream);
+  if (e == hipSuccess) e = hipStreamSynchronize((hipStream_t)stream);
+  if (e != hipSuccess) {
+    free(h);
+    return hip_fail(e, "copy of the loss buckets");
+  }
+  for (int32_t b = 0; b < n_buckets; ++b) {
+    const double sum = h[2 * b], cnt = h[2 * b + 1];
+    if (!__builtin_isfinite(sum) || !__builtin_isfinite(cnt)) {
+      free(h);
+      return failf(W2V_ENONFINITE,
+                   "loss bucket %d is not finite (sum %g over %g input words): a NaN "
+                   "or Inf reached the rows its minibatches read",
+                   (int)b, sum, cnt);
+    }
+  }
+  free(h);
+  return ok();
 }
 
 int w2v_build_tables(const int64_t* counts, int32_t V, double neg_power,

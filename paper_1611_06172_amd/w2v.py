@@ -32,6 +32,7 @@ EHIP = -2
 ENOMEM = -3
 EUNSUPPORTED = -4
 EDEVICE_FLAG = -5
+ENONFINITE = -6
 
 
 class W2VError(RuntimeError):
@@ -56,6 +57,8 @@ def lib():
     L.w2v_init.restype = ctypes.c_int
     L.w2v_device_status.argtypes = [_vp]
     L.w2v_device_status.restype = ctypes.c_int
+    L.w2v_check_loss.argtypes = [_vp, _i32, _vp]
+    L.w2v_check_loss.restype = ctypes.c_int
     L.w2v_build_tables.argtypes = [_vp, _i32, _f64, _f64, _vp, _i64, _vp]
     L.w2v_build_tables.restype = ctypes.c_int
     L.w2v_train_epoch.argtypes = [
@@ -191,6 +194,15 @@ def device_status(stream=None):
     kernel of the library skipped work for an id outside [0, V) since this
     was last reported (w2v_device_status)."""
     _check(lib().w2v_device_status(_stream(stream)))
+
+
+def check_loss(loss_buckets, stream=None):
+    """Waits for the stream, then raises W2VError (code ENONFINITE) naming the
+    first loss bucket whose sum or count is NaN or Inf (w2v_check_loss)."""
+    import torch
+    _dev(loss_buckets, torch.float64, "loss_buckets", 2)
+    _check(lib().w2v_check_loss(_ptr(loss_buckets), loss_buckets.shape[0],
+                                _stream(stream)))
 
 
 def default_inflight(D: int, window: int = 5, K: int = 5, *, V: int,

@@ -30,7 +30,7 @@ def test_exports_every_declared_symbol():
 
 
 def test_version():
-    assert w2v.version() == 102
+    assert w2v.version() == 103
 
 
 @pytest.mark.parametrize("seed,power,t,size", [
@@ -219,3 +219,11 @@ def test_step_batch_sorted_workspace_rejects_invalid_shapes():
     for args in ((-1, 2, 1, 10, 8), (4, -1, 1, 10, 8), (4, 2, -1, 10, 8),
                  (4, 2, 1, 0, 8), (4, 2, 1, 10, 0)):
         assert L.w2v_step_batch_sorted_workspace_bytes(*args) == 0
+
+
+def test_check_loss_rejects():
+    L = w2v.lib()
+    assert L.w2v_check_loss(None, -1, None) == w2v.EINVAL
+    assert "n_buckets" in L.w2v_last_error().decode()
+    assert L.w2v_check_loss(None, 3, None) == w2v.EINVAL
+    assert "NULL" in L.w2v_last_error().decode()
