@@ -557,7 +557,8 @@ def row_rmw_bench(args):
     for the last `atomic_rows` of a step, added with fp32 atomics. Rows of
     D = 300 floats at ld = 320 in a 1e6-row matrix. Also uniform random ids.
     Bytes are counted as the epoch's algorithmic bytes: every row read and
-    written once (2 x 1200 B)."""
+    written once (2 x 1200 B). Then the snapshot batch's rows (kernel-test
+    shape) with every update an fp32 atomic, against uniform ids."""
     import ctypes
     import numpy as np
     import torch
@@ -619,6 +620,38 @@ def row_rmw_bench(args):
         results[label] = {"ms": round(ms, 3), "GBs": round(gbs, 1)}
         print(f"[bench] row-rmw {label}: {ms:.2f} ms, {gbs:.0f} GB/s", file=sys.stderr,
               flush=True)
+    # The snapshot batch's shape with every update atomic: the 16 rows of each
+    # of 65,536 kernel-test minibatches (Zipf(1.0) ids over 1e5 words, as
+    # w2v_step_batch adds them) against the same number of uniform ids, one
+    # minibatch per wavefront; the rate of the memory side's atomics with and
+    # without the head rows' contention.
+    Vk, Bk, Rk = 100_000, 65536, 16
+    t, c, n = inputs.kernel_batch(Bk, 10, 5, Vk, 1.0, 3)
+    kt_ids = torch.from_numpy(np.ascontiguousarray(
+        np.concatenate([c, t[:, None], n], 1).astype(np.int32).reshape(-1))).to(dev)
+    kt_uniform = torch.randint(0, Vk, (Bk * Rk,), generator=g, device=dev, dtype=torch.int32)
+    Mk = w2v.alloc_matrix(Vk, D, dev)
+    per_row = (4 * D + 63) // 64     # 64-byte requests of one row's fp32 atomics
+    for label, ids in (("kernel-test rows, all atomic", kt_ids),
+                       ("uniform rows (V 1e5), all atomic", kt_uniform)):
+        def call():
+            rc = L.w2v_measure_row_rmw(Mk.data_ptr(), Vk, D, Mk.stride(0), ids.data_ptr(),
+                                       Bk, Rk, Rk, Bk, stream.cuda_stream)
+            if rc != 0:
+                raise RuntimeError(f"w2v_measure_row_rmw failed ({rc})")
+        call()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(max(args.steps, 1)):
+            call()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / max(args.steps, 1)
+        rate = Bk * Rk * per_row / (ms * 1e-3)
+        results[label] = {"ms": round(ms, 3), "atomic_requests_per_s": float(f"{rate:.4g}")}
+        print(f"[bench] row-rmw {label}: {ms:.3f} ms, {rate / 1e9:.2f} G requests/s",
+              file=sys.stderr, flush=True)
     head = results["epoch rows, 3 of 12 atomic"]
     result = {
         "metric": "GB/s, random row read-modify-write (the epoch's row accesses without "
