@@ -36,6 +36,28 @@ def test_vocab_matches_reference(V_raw, T, min_count):
     assert np.array_equal(out["corpus"].cpu().numpy(), corpus)
 
 
+@pytest.mark.parametrize("kind", ["sorted", "constant", "two_bins_alternating"])
+def test_vocab_unusual_streams(kind):
+    """Streams whose ids are not spread over the chunks: sorted ids (each
+    chunk holds one or two id ranges, so most segments are empty and a few
+    fill whole chunks), one id repeated, and two ids from different ranges
+    alternating; bit for bit against the reference."""
+    import torch
+    V_raw, T = 100_000, 3_000_017
+    if kind == "sorted":
+        raw = np.sort(inputs.zipf_ids(T, V_raw, 1.0, 8)).astype(np.int32)
+    elif kind == "constant":
+        raw = np.full(T, 65_537, np.int32)
+    else:
+        raw = np.where(np.arange(T) % 2 == 0, 7, 99_999).astype(np.int32)
+    ranked, rank_of, V, corpus = oracle.build_vocab(raw, V_raw, 2)
+    out = w2v.build_vocab(torch.from_numpy(raw).cuda(), V_raw, 2)
+    assert out["V"] == V
+    assert np.array_equal(out["ranked_counts"].cpu().numpy(), ranked)
+    assert np.array_equal(out["rank_of"].cpu().numpy(), rank_of)
+    assert np.array_equal(out["corpus"].cpu().numpy(), corpus)
+
+
 def test_ranked_corpus_trains_with_update_tiers():
     """A shuffled-id stream ranked on the GPU: its tables, conflict-model
     thresholds and a concurrent epoch, against the serialised epoch of the
