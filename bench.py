@@ -12,6 +12,7 @@ subsampling), the roofline of the epoch kernel from HIP events recorded on its
 stream, and the CPU oracle's rate on a bounded sample of the same workload.
 """
 import argparse
+import dataclasses
 import hashlib
 import re
 import json
@@ -21,6 +22,11 @@ import time
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
+
+from paper_1611_06172_amd import configs  # noqa: E402
+
+LV = configs.LargeVocab()     # the throughput workload
+KT = configs.KernelTest()     # the snapshot-batch workload
 
 HBM_PEAK_GBS = 8000.0   # MI355X HBM3E, 8 TB/s
 METRIC = "Mwords/sec at V=1M D=300 K=5 window=5 (1 GPU); achieved HBM GB/s"
@@ -89,12 +95,12 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=3)
     ap.add_argument("--warmup", type=int, default=1)
-    ap.add_argument("--tokens", type=float, default=1e9)
-    ap.add_argument("--vocab", type=int, default=1_000_000)
-    ap.add_argument("--dim", type=int, default=300)
-    ap.add_argument("--negative", type=int, default=5)
-    ap.add_argument("--window", type=int, default=5)
-    ap.add_argument("--sample", type=float, default=1e-4)
+    ap.add_argument("--tokens", type=float, default=float(LV.T))
+    ap.add_argument("--vocab", type=int, default=LV.V)
+    ap.add_argument("--dim", type=int, default=LV.D)
+    ap.add_argument("--negative", type=int, default=LV.K)
+    ap.add_argument("--window", type=int, default=LV.window)
+    ap.add_argument("--sample", type=float, default=LV.sample)
     ap.add_argument("--max-inflight", type=int, default=0)
     ap.add_argument("--group", type=int, default=1,
                     help="consecutive targets sharing one draw of negatives "
@@ -166,15 +172,16 @@ def main():
     torch.cuda.set_device(dev)
     V, D, K, W = args.vocab, args.dim, args.negative, args.window
     T = int(args.tokens)
-    L = 1000
+    L = LV.sentence
+    cfg = dataclasses.replace(LV, T=T, V=V, D=D, K=K, window=W, sample=args.sample)
 
     t0 = time.time()
-    corpus = inputs.zipf_corpus_hashed(T, V, 1.07, 6, dev)
+    corpus = inputs.zipf_corpus_hashed(T, V, LV.zipf_s, LV.corpus_seed, dev)
     counts = torch.bincount(corpus, minlength=V).cpu().numpy().astype(np.int64)
-    table_h, thr_h = w2v.build_tables(counts, 0.75, args.sample, 10**8)
+    table_h, thr_h = w2v.build_tables(counts, 0.75, args.sample, LV.table_size)
     table = torch.from_numpy(table_h).to(dev)
     thr = torch.from_numpy(thr_h.view(np.int32)).to(dev)
-    M_in0 = inputs.init_matrix(V, D, "uniform", 2)
+    M_in0 = inputs.init_matrix(V, D, "uniform", LV.init_seed)
     # rows padded to whole 128-byte lines (ld = 320 floats at D = 300)
     M_in = w2v.alloc_matrix(V, D, dev, torch.from_numpy(M_in0))
     M_out = w2v.alloc_matrix(V, D, dev)
@@ -210,8 +217,8 @@ def main():
 
     def step(i, algorithm=args.algorithm):
         w2v.train_epoch(corpus, M_in, M_out, table, thr, window=W, K=K,
-                        alpha0=0.025, min_alpha_frac=1e-4, epoch=i,
-                        n_epochs=n_epochs, seed=1234, sentence_len=L,
+                        alpha0=LV.alpha0, min_alpha_frac=1e-4, epoch=i,
+                        n_epochs=n_epochs, seed=LV.sampling_seed, sentence_len=L,
                         stats=stats, max_inflight=args.max_inflight,
                         hot_rows=hot, split_rows=split, workspace=workspace,
                         algorithm=algorithm, group=args.group)
@@ -285,6 +292,7 @@ def main():
             "split_rows": int(split),
             "minibatches_per_step": int(n_mb), "mean_inputs_per_minibatch":
                 round(sum_n / max(n_mb, 1), 4), "retained_fraction": round(n_mb / raw, 4),
+            "workload_config": json.loads(configs.to_json(cfg)),
             "steps_are": (f"epochs {args.warmup}..{args.warmup + args.steps - 1} of a "
                           f"{n_epochs}-epoch schedule (alpha decays over the schedule; each "
                           f"epoch continues from the previous one's matrices), after "
@@ -356,7 +364,7 @@ def main():
         o_in = M_in0.copy()
         o_out = np.zeros((V, D), dtype=np.float32)
         s = oracle.Sampling(sample_corpus, table_h, thr_h, window=W, K=K,
-                            sentence_len=L, seed=1234, n_epochs=1)
+                            sentence_len=L, seed=LV.sampling_seed, n_epochs=1)
         if args.algorithm == "pairwise":
             run = lambda: oracle.pairwise_train_epoch(s, o_in, o_out)  # noqa: E731
         elif args.group > 1:
@@ -390,10 +398,10 @@ def kernel_test(args):
 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    B, N, K, V, D = 65536, 10, 5, 100_000, 300
-    t, c, n = inputs.kernel_batch(B, N, K, V, 1.0, 3)
-    Mi0 = inputs.init_matrix(V, D, "normal", 4)
-    Mo0 = inputs.init_matrix(V, D, "normal", 104)
+    B, N, K, V, D = KT.B, KT.N, KT.K, KT.V, KT.D
+    t, c, n = inputs.kernel_batch(B, N, K, V, KT.zipf_s, KT.ids_seed)
+    Mi0 = inputs.init_matrix(V, D, "normal", KT.init_seed)
+    Mo0 = inputs.init_matrix(V, D, "normal", KT.init_seed + 100)
     M_in = w2v.alloc_matrix(V, D, dev, torch.from_numpy(Mi0))
     M_out = w2v.alloc_matrix(V, D, dev, torch.from_numpy(Mo0))
     T, C, Ng = (torch.from_numpy(x).to(dev) for x in (t, c, n))
@@ -403,9 +411,9 @@ def kernel_test(args):
         src.fill_(1.0)
         dst = src.clone()
         del src, dst
-    ws = w2v.step_batch(T, C, Ng, M_in, M_out, 0.025, D=D, sorted=srt)  # allocates
+    ws = w2v.step_batch(T, C, Ng, M_in, M_out, KT.alpha, D=D, sorted=srt)  # allocates
     for _ in range(max(args.warmup, 0)):
-        w2v.step_batch(T, C, Ng, M_in, M_out, 0.025, D=D, workspace=ws, sorted=srt)
+        w2v.step_batch(T, C, Ng, M_in, M_out, KT.alpha, D=D, workspace=ws, sorted=srt)
     steps = max(args.steps, 1) * 20   # a batch takes about a millisecond
     stream = torch.cuda.current_stream()
     evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
@@ -414,7 +422,7 @@ def kernel_test(args):
     t_start = time.perf_counter()
     for i in range(steps):
         evs[i][0].record(stream)
-        w2v.step_batch(T, C, Ng, M_in, M_out, 0.025, D=D, workspace=ws, sorted=srt)
+        w2v.step_batch(T, C, Ng, M_in, M_out, KT.alpha, D=D, workspace=ws, sorted=srt)
         evs[i][1].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t_start
@@ -450,7 +458,7 @@ def kernel_test(args):
         import oracle
         bs = B
         _, c_dt, cpu, n_cpu = on_one_core(lambda: oracle.step_batch(
-            t[:bs], c[:bs], n[:bs], Mi0, Mo0, 0.025, D=D, with_scale=False))
+            t[:bs], c[:bs], n[:bs], Mi0, Mo0, KT.alpha, D=D, with_scale=False))
         result["cpu_baseline"] = {
             "value": round(bs / c_dt / 1e6, 5), "unit": "Mminibatches/s",
             "cores": 1, "kind": "oracle",

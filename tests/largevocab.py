@@ -8,18 +8,19 @@ held-out score is the mean SGNS loss per input word of 20,000 minibatches
 drawn independently of the corpus."""
 import numpy as np
 
-from paper_1611_06172_amd import inputs
+from paper_1611_06172_amd import configs, inputs
 
-V, D, K, WINDOW, SAMPLE = 1_000_000, 300, 5, 5, 1e-4
-T = 100_000_000
-CORPUS_SEED = 6          # the benchmark's corpus seed
-SEED = 1234              # the benchmark's sampling seed
+CFG = configs.LargeVocab()
+V, D, K, WINDOW, SAMPLE = CFG.V, CFG.D, CFG.K, CFG.window, CFG.sample
+T = 100_000_000          # the prefix the oracle follows
+CORPUS_SEED = CFG.corpus_seed
+SEED = CFG.sampling_seed
 N_BUCKETS = 10
 
 
 def corpus(device="cpu"):
     """int32 torch tensor of the T tokens on `device`."""
-    return inputs.zipf_corpus_hashed(T, V, 1.07, CORPUS_SEED, device)
+    return inputs.zipf_corpus_hashed(T, V, CFG.zipf_s, CORPUS_SEED, device)
 
 
 def counts(corpus_np):
@@ -27,7 +28,7 @@ def counts(corpus_np):
 
 
 def init_in():
-    return inputs.init_matrix(V, D, "uniform", 2)
+    return inputs.init_matrix(V, D, "uniform", CFG.init_seed)
 
 
 def heldout_ids(table):

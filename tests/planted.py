@@ -12,29 +12,31 @@ about 1%).
 """
 import numpy as np
 
-from paper_1611_06172_amd import inputs
+from paper_1611_06172_amd import configs, inputs
 
-V = 71_290
-T = 17_000_000
-N_TOPICS = 100
-D = 200
-WINDOW = 8
-K = 25
-SAMPLE = 1e-4
-EPOCHS = 5
-ALPHA0 = 0.025
-SENTENCE = 1000
-CORPUS_SEED = 5
-INIT_SEED = 2
-SAMPLING_SEED = 17
-TABLE_SIZE = 10**8
+CFG = configs.Planted()
+V = CFG.V
+T = CFG.T
+N_TOPICS = CFG.n_topics
+D = CFG.D
+WINDOW = CFG.window
+K = CFG.K
+SAMPLE = CFG.sample
+EPOCHS = CFG.epochs
+ALPHA0 = CFG.alpha0
+SENTENCE = CFG.sentence
+CORPUS_SEED = CFG.corpus_seed
+INIT_SEED = CFG.init_seed
+SAMPLING_SEED = CFG.sampling_seed
+TABLE_SIZE = CFG.table_size
 # Sentence-aligned token counts inside epoch 0 at which the score is also
 # taken (the score saturates later in the run).
 CHECKPOINTS = (100_000, 300_000, 1_000_000)
 
 
 def corpus(T_=T):
-    return inputs.planted_topic_corpus(T_, V, N_TOPICS, 1.0, 0.05, CORPUS_SEED)
+    return inputs.planted_topic_corpus(T_, V, N_TOPICS, CFG.topic_zipf_s, CFG.switch,
+                                       CORPUS_SEED)
 
 
 def init_in():

@@ -14,17 +14,20 @@ import numpy as np
 import pytest
 
 import oracle
-from paper_1611_06172_amd import inputs, w2v
+from paper_1611_06172_amd import configs, inputs, w2v
 from gpu_util import thresh_dev, to_dev
 
 pytestmark = pytest.mark.gpu
 
 
-def tiny_config(T=200_000, V=1000, D=64, seed=1):
-    corpus = inputs.zipf_ids(T, V, 1.0, seed)
-    table, _ = oracle.build_tables(inputs.word_counts(corpus, V), 0.75, 0.0, 10**8,
+TINY = configs.Tiny()
+
+
+def tiny_config(T=TINY.T, V=TINY.V, D=TINY.D, seed=TINY.corpus_seed):
+    corpus = inputs.zipf_ids(T, V, TINY.zipf_s, seed)
+    table, _ = oracle.build_tables(inputs.word_counts(corpus, V), 0.75, TINY.sample, 10**8,
                                    want_thresh=False)
-    M_in = inputs.init_matrix(V, D, "uniform", 2)
+    M_in = inputs.init_matrix(V, D, "uniform", TINY.init_seed)
     M_out = inputs.init_matrix(V, D, "zeros", 0)
     return corpus, table, M_in, M_out
 
