@@ -8,14 +8,18 @@ on prefixes of the benchmark's corpus that the oracle can follow:
 * as the benchmark launches it (every sentence of 1e7 tokens, 2048 in
   flight): minibatch and input-word counts equal the oracle's exactly, rows
   no minibatch touches stay bitwise unchanged, the matrices stay finite and
-  the training loss falls along the epoch.
+  the training loss falls along the epoch;
+* the whole 1e9-token corpus as the benchmark trains it: per tenth of the
+  corpus the epoch's minibatch and input-word counts equal the sampling
+  export's over the same tenth, the export equals the oracle bit for bit on
+  sampled ranges at the start, middle and end, and the loss falls.
 """
 import numpy as np
 import pytest
 
 import oracle
-from gpu_util import to_dev
-from paper_1611_06172_amd import inputs, w2v
+from gpu_util import assert_same_minibatches, gpu_minibatches, to_dev
+from paper_1611_06172_amd import configs, inputs, w2v
 from test_gpu_train_epoch import rel_row_error
 
 pytestmark = pytest.mark.gpu
@@ -93,3 +97,60 @@ def test_bench_launch_configuration_on_a_prefix():
     assert np.isfinite(gi).all() and np.isfinite(go).all()
     loss = lb[:, 0] / lb[:, 1]
     assert loss[-1] < 0.9 * loss[0]
+
+
+def test_whole_corpus_in_the_bench_launch():
+    import torch
+    cfg = configs.LargeVocab()
+    T, seed = cfg.T, cfg.sampling_seed
+    print(f"[full] drawing {T} tokens", flush=True)
+    corpus = inputs.zipf_corpus_hashed(T, V, cfg.zipf_s, cfg.corpus_seed, "cuda")
+    counts = torch.bincount(corpus, minlength=V).cpu().numpy().astype(np.int64)
+    table, thr = oracle.build_tables(counts, 0.75, cfg.sample, cfg.table_size)
+    g_table, g_thr = w2v.build_tables(counts, 0.75, cfg.sample, cfg.table_size)
+    assert np.array_equal(table, g_table) and np.array_equal(thr, g_thr)
+    table_d, thr_d = to_dev(table), torch.from_numpy(thr.view(np.int32)).cuda()
+    inflight = w2v.default_inflight(D, cfg.window, cfg.K, V=V)
+    hot = w2v.hot_rows(counts, inflight=inflight, tol=0.5)
+    split = min(2, w2v.hot_rows(counts, inflight=inflight, tol=128.0))
+    gi = w2v.alloc_matrix(V, D, "cuda",
+                          torch.from_numpy(inputs.init_matrix(V, D, "uniform", cfg.init_seed)))
+    go = w2v.alloc_matrix(V, D, "cuda")
+    stats = torch.zeros(5, dtype=torch.int64, device="cuda")
+    lb = torch.zeros((10, 2), dtype=torch.float64, device="cuda")
+    print(f"[full] epoch: inflight {inflight}, hot {hot}, split {split}", flush=True)
+    w2v.train_epoch(corpus, gi, go, table_d, thr_d, window=cfg.window, K=cfg.K,
+                    seed=seed, stats=stats, loss_buckets=lb, max_inflight=inflight,
+                    hot_rows=hot, split_rows=split)
+    torch.cuda.synchronize()
+    assert bool(torch.isfinite(gi[:, :D]).all()) and bool(torch.isfinite(go[:, :D]).all())
+    st, lbh = stats.cpu().numpy(), lb.cpu().numpy()
+    kw = dict(V=V, window=cfg.window, K=cfg.K, seed=seed)
+    step = T // 10
+    n_tot = in_tot = 0
+    for b in range(10):
+        mb = w2v.debug_minibatches(corpus, table_d, thr_d, pos_begin=b * step,
+                                   pos_end=(b + 1) * step, **kw)
+        keep = mb["targets"] >= 0
+        n_b = int(keep.sum())
+        in_b = int(((mb["ctx"] >= 0).sum(1) * keep).sum())
+        del mb
+        assert lbh[b, 1] == in_b, (b, lbh[b, 1], in_b)
+        n_tot += n_b
+        in_tot += in_b
+    print(f"[full] {n_tot} minibatches, {in_tot} input words", flush=True)
+    assert st[0] == n_tot and st[1] == in_tot and st[2] == T and st[3] == 0
+    corpus_h = corpus.cpu().numpy()
+    for b0 in (0, T // 2, T - 200_000):
+        o = oracle.minibatches(oracle.Sampling(corpus_h, table, thr, window=cfg.window,
+                                               K=cfg.K, seed=seed, pos_begin=b0,
+                                               pos_end=b0 + 200_000))
+        g = gpu_minibatches(w2v.debug_minibatches(corpus, table_d, thr_d, pos_begin=b0,
+                                                  pos_end=b0 + 200_000, **kw), b0)
+        assert_same_minibatches(g, o)
+    # the loss per input word starts at (K + 1) ln 2 (M_out = 0) and every
+    # later tenth is below the first one
+    loss = lbh[:, 0] / lbh[:, 1]
+    print(f"[full] loss per tenth {np.round(loss, 4).tolist()}", flush=True)
+    assert loss[0] < (cfg.K + 1) * np.log(2.0)
+    assert loss[1:].max() < loss[0] and loss[-1] < loss[0] - 0.1
