@@ -241,6 +241,11 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t_start
     kern_ms = [a.elapsed_time(b) for a, b in evs]
+    # a throughput of a diverged run is no measurement of the method
+    if not (bool(torch.isfinite(M_in).all()) and bool(torch.isfinite(M_out).all())):
+        raise RuntimeError("the timed epochs left non-finite values in the matrices "
+                           "(Hogwild divergence at this concurrency and learning rate); "
+                           "no throughput is reported")
     st = stats.cpu().numpy().astype(np.float64) / args.steps
     print(f"[bench] timed {args.steps} steps in {wall:.2f}s; per launch "
           f"{[round(x, 1) for x in kern_ms]} ms", file=sys.stderr, flush=True)

@@ -163,7 +163,12 @@ int32_t w2v_hot_rows(const int64_t* counts, int32_t V, double neg_power,
  * of the vocabulary, so that a small vocabulary is not trained mostly from
  * stale rows; Hogwild staleness is what separates the concurrent epoch from
  * the sequential one (Sec. 1.1). At V = 10^6, window 5, K = 5 the cap
- * (15,625) is above what the GPU holds. */
+ * (15,625) is above what the GPU holds. A second cap, 131072 / (K + 1)
+ * (2016 at K = 64), bounds how many concurrent sentences update the rows of
+ * the words most often drawn as negatives, each from the row as it was
+ * before the others' updates: at K = 64, D = 100 and alpha 0.025 the epoch
+ * over a Zipf(1.07) vocabulary of 10^6 words learned with up to 2048
+ * sentences in flight and diverged (NaN) with 2560. */
 int64_t w2v_default_inflight(int32_t V, int32_t D, int32_t window, int32_t K,
                              int32_t group);
 

@@ -219,6 +219,25 @@ static int64_t vocab_inflight_cap(int64_t V, int window, int K, int group) {
   return cap > 0 ? cap : 1;
 }
 
+// Concurrency cap of a default launch for K negatives: 131072 / (K + 1)
+// (2016 at K = 64; above what the GPU holds for K <= 40). Under a Zipf law
+// the most frequent words are drawn as negatives by most minibatches once K
+// is large, so the rows of those words take one update from nearly every
+// sentence in flight, each computed from the row as it was before the
+// others landed; past some number of such concurrent updates the Hogwild
+// epoch overshoots and diverges. Measured on 1e8 tokens over 10^6 words
+// (Zipf(1.07), window 5, alpha 0.025, the conflict model's atomic rows and
+// split head): at D = 100, K = 64 finite and learning with 1024, 1536 and
+// 2048 sentences in flight, NaN with 2560 and 3072; at D = 300, K = 64
+// finite up to 3072; at K <= 15 finite at every concurrency the GPU holds.
+// (At twice that learning rate, K = 15 diverged with 3072 in flight: the
+// bound is the method's, and a caller who raises alpha or the concurrency
+// checks the loss with w2v_check_loss.)
+static int64_t negatives_inflight_cap(int K) {
+  const int64_t cap = (int64_t)131072 / ((int64_t)K + 1);
+  return cap > 0 ? cap : 1;
+}
+
 // A default launch also runs its sentences in at least kMinRounds rounds of
 // the persistent grid, so that most sentences start from a model that the
 // earlier ones have moved: with every sentence of a short range in flight at
@@ -238,7 +257,7 @@ using namespace w2v;
 
 extern "C" {
 
-int w2v_version(void) { return 103; }
+int w2v_version(void) { return 104; }
 
 const char* w2v_last_error(void) { return g_error; }
 
@@ -324,7 +343,9 @@ int64_t w2v_default_inflight(int32_t V, int32_t D, int32_t window, int32_t K,
   if (per_cu <= 0 || cus <= 0) return fail(W2V_EHIP, "device query failed");
   ok();
   const int64_t full = (int64_t)per_cu * cus;
-  const int64_t cap = vocab_inflight_cap(V, window, K, group);
+  int64_t cap = vocab_inflight_cap(V, window, K, group);
+  const int64_t ncap = negatives_inflight_cap(K);
+  if (ncap < cap) cap = ncap;
   return full < cap ? full : cap;
 }
 
@@ -467,6 +488,8 @@ static int train_epoch_impl(const int32_t* corpus, int64_t T, int64_t pos_begin,
     grid = (int64_t)(per_cu > 0 ? per_cu : 1) * (cus > 0 ? cus : 1);
     const int64_t cap = vocab_inflight_cap(V, window, K, group);
     if (grid > cap) grid = cap;
+    const int64_t ncap = negatives_inflight_cap(K);
+    if (grid > ncap) grid = ncap;
     const int64_t rcap = rounds_inflight_cap(n_sent);
     if (grid > rcap) grid = rcap;
   }

@@ -9,10 +9,12 @@ on prefixes of the benchmark's corpus that the oracle can follow:
   flight): minibatch and input-word counts equal the oracle's exactly, rows
   no minibatch touches stay bitwise unchanged, the matrices stay finite and
   the training loss falls along the epoch;
-* the whole 1e9-token corpus as the benchmark trains it: per tenth of the
-  corpus the epoch's minibatch and input-word counts equal the sampling
-  export's over the same tenth, the export equals the oracle bit for bit on
-  sampled ranges at the start, middle and end, and the loss falls.
+* the whole 1e9-token corpus as the benchmark trains it, and every cell of
+  the shape sweep (D in {100, 300, 600} x K in {5, 15, 64}) on its 1e8-token
+  corpus: per tenth of the corpus the epoch's input-word count equals the
+  sampling export's over the same tenth (and the totals), the export equals
+  the oracle bit for bit on sampled ranges at the start, middle and end, the
+  matrices stay finite and the loss falls.
 """
 import numpy as np
 import pytest
@@ -99,33 +101,39 @@ def test_bench_launch_configuration_on_a_prefix():
     assert loss[-1] < 0.9 * loss[0]
 
 
-def test_whole_corpus_in_the_bench_launch():
+def full_run(T, D_, K_, print_loss=False):
+    """Trains the first T tokens of the throughput corpus for one epoch as
+    bench.py does (tables from their counts, the default concurrency, the
+    conflict model's atomic rows at tol 0.5 and at most two split rows),
+    then checks it against the sampling export per tenth of the range and
+    the export against the oracle on three sampled ranges."""
     import torch
     cfg = configs.LargeVocab()
-    T, seed = cfg.T, cfg.sampling_seed
-    print(f"[full] drawing {T} tokens", flush=True)
+    seed = cfg.sampling_seed
+    print(f"[full] drawing {T} tokens, D {D_}, K {K_}", flush=True)
     corpus = inputs.zipf_corpus_hashed(T, V, cfg.zipf_s, cfg.corpus_seed, "cuda")
     counts = torch.bincount(corpus, minlength=V).cpu().numpy().astype(np.int64)
     table, thr = oracle.build_tables(counts, 0.75, cfg.sample, cfg.table_size)
     g_table, g_thr = w2v.build_tables(counts, 0.75, cfg.sample, cfg.table_size)
     assert np.array_equal(table, g_table) and np.array_equal(thr, g_thr)
     table_d, thr_d = to_dev(table), torch.from_numpy(thr.view(np.int32)).cuda()
-    inflight = w2v.default_inflight(D, cfg.window, cfg.K, V=V)
-    hot = w2v.hot_rows(counts, inflight=inflight, tol=0.5)
-    split = min(2, w2v.hot_rows(counts, inflight=inflight, tol=128.0))
-    gi = w2v.alloc_matrix(V, D, "cuda",
-                          torch.from_numpy(inputs.init_matrix(V, D, "uniform", cfg.init_seed)))
-    go = w2v.alloc_matrix(V, D, "cuda")
+    inflight = w2v.default_inflight(D_, cfg.window, K_, V=V)
+    hot = w2v.hot_rows(counts, inflight=inflight, K=K_, tol=0.5)
+    split = min(2, w2v.hot_rows(counts, inflight=inflight, K=K_, tol=128.0))
+    gi = w2v.alloc_matrix(V, D_, "cuda",
+                          torch.from_numpy(inputs.init_matrix(V, D_, "uniform", cfg.init_seed)))
+    go = w2v.alloc_matrix(V, D_, "cuda")
     stats = torch.zeros(5, dtype=torch.int64, device="cuda")
     lb = torch.zeros((10, 2), dtype=torch.float64, device="cuda")
     print(f"[full] epoch: inflight {inflight}, hot {hot}, split {split}", flush=True)
-    w2v.train_epoch(corpus, gi, go, table_d, thr_d, window=cfg.window, K=cfg.K,
+    w2v.train_epoch(corpus, gi, go, table_d, thr_d, window=cfg.window, K=K_,
                     seed=seed, stats=stats, loss_buckets=lb, max_inflight=inflight,
                     hot_rows=hot, split_rows=split)
     torch.cuda.synchronize()
-    assert bool(torch.isfinite(gi[:, :D]).all()) and bool(torch.isfinite(go[:, :D]).all())
+    assert bool(torch.isfinite(gi).all()) and bool(torch.isfinite(go).all())
+    del gi, go
     st, lbh = stats.cpu().numpy(), lb.cpu().numpy()
-    kw = dict(V=V, window=cfg.window, K=cfg.K, seed=seed)
+    kw = dict(V=V, window=cfg.window, K=K_, seed=seed)
     step = T // 10
     n_tot = in_tot = 0
     for b in range(10):
@@ -143,7 +151,7 @@ def test_whole_corpus_in_the_bench_launch():
     corpus_h = corpus.cpu().numpy()
     for b0 in (0, T // 2, T - 200_000):
         o = oracle.minibatches(oracle.Sampling(corpus_h, table, thr, window=cfg.window,
-                                               K=cfg.K, seed=seed, pos_begin=b0,
+                                               K=K_, seed=seed, pos_begin=b0,
                                                pos_end=b0 + 200_000))
         g = gpu_minibatches(w2v.debug_minibatches(corpus, table_d, thr_d, pos_begin=b0,
                                                   pos_end=b0 + 200_000, **kw), b0)
@@ -152,5 +160,21 @@ def test_whole_corpus_in_the_bench_launch():
     # later tenth is below the first one
     loss = lbh[:, 0] / lbh[:, 1]
     print(f"[full] loss per tenth {np.round(loss, 4).tolist()}", flush=True)
-    assert loss[0] < (cfg.K + 1) * np.log(2.0)
-    assert loss[1:].max() < loss[0] and loss[-1] < loss[0] - 0.1
+    assert loss[0] < (K_ + 1) * np.log(2.0)
+    assert loss[1:].max() < loss[0]
+    return loss
+
+
+def test_whole_corpus_in_the_bench_launch():
+    """The 1e9-token throughput workload (D = 300, K = 5), as bench.py runs it."""
+    cfg = configs.LargeVocab()
+    loss = full_run(cfg.T, cfg.D, cfg.K)
+    assert loss[-1] < loss[0] - 0.1
+
+
+@pytest.mark.parametrize("D_,K_", [(d, k) for d in configs.Sweep().dims
+                                   for k in configs.Sweep().negatives])
+def test_sweep_cell_at_full_size(D_, K_):
+    """Each cell of the shape sweep on its 1e8-token corpus, as bench.py
+    --tokens 1e8 --dim D --negative K runs it."""
+    full_run(configs.Sweep().T, D_, K_)

@@ -30,7 +30,7 @@ def test_exports_every_declared_symbol():
 
 
 def test_version():
-    assert w2v.version() == 103
+    assert w2v.version() == 104
 
 
 @pytest.mark.parametrize("seed,power,t,size", [
