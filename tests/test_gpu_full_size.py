@@ -101,7 +101,7 @@ def test_bench_launch_configuration_on_a_prefix():
     assert loss[-1] < 0.9 * loss[0]
 
 
-def full_run(T, D_, K_, print_loss=False):
+def full_run(T, D_, K_, algorithm="hogbatch", group=1):
     """Trains the first T tokens of the throughput corpus for one epoch as
     bench.py does (tables from their counts, the default concurrency, the
     conflict model's atomic rows at tol 0.5 and at most two split rows),
@@ -117,9 +117,11 @@ def full_run(T, D_, K_, print_loss=False):
     g_table, g_thr = w2v.build_tables(counts, 0.75, cfg.sample, cfg.table_size)
     assert np.array_equal(table, g_table) and np.array_equal(thr, g_thr)
     table_d, thr_d = to_dev(table), torch.from_numpy(thr.view(np.int32)).cuda()
-    inflight = w2v.default_inflight(D_, cfg.window, K_, V=V)
+    inflight = w2v.default_inflight(D_, cfg.window, K_, V=V, group=group)
     hot = w2v.hot_rows(counts, inflight=inflight, K=K_, tol=0.5)
     split = min(2, w2v.hot_rows(counts, inflight=inflight, K=K_, tol=128.0))
+    if algorithm == "pairwise":
+        split = 0   # partial rows serve the HogBatch kernels only
     gi = w2v.alloc_matrix(V, D_, "cuda",
                           torch.from_numpy(inputs.init_matrix(V, D_, "uniform", cfg.init_seed)))
     go = w2v.alloc_matrix(V, D_, "cuda")
@@ -128,7 +130,7 @@ def full_run(T, D_, K_, print_loss=False):
     print(f"[full] epoch: inflight {inflight}, hot {hot}, split {split}", flush=True)
     w2v.train_epoch(corpus, gi, go, table_d, thr_d, window=cfg.window, K=K_,
                     seed=seed, stats=stats, loss_buckets=lb, max_inflight=inflight,
-                    hot_rows=hot, split_rows=split)
+                    hot_rows=hot, split_rows=split, algorithm=algorithm, group=group)
     torch.cuda.synchronize()
     assert bool(torch.isfinite(gi).all()) and bool(torch.isfinite(go).all())
     del gi, go
@@ -178,3 +180,14 @@ def test_sweep_cell_at_full_size(D_, K_):
     """Each cell of the shape sweep on its 1e8-token corpus, as bench.py
     --tokens 1e8 --dim D --negative K runs it."""
     full_run(configs.Sweep().T, D_, K_)
+
+
+@pytest.mark.parametrize("algorithm,group", [("hogbatch", 2), ("hogbatch", 4),
+                                             ("pairwise", 1), ("hogbatch_immediate", 1)])
+def test_other_variants_at_full_size(algorithm, group):
+    """The variants bench.py measures beside the headline (negatives shared by
+    2 and 4 targets, Algorithm 1, write-back at the end of each minibatch) on
+    the 1e8-token corpus in their bench launch: the same targets and input
+    words as the sampling export, finite matrices, a falling loss."""
+    full_run(configs.Sweep().T, configs.LargeVocab().D, configs.LargeVocab().K,
+             algorithm=algorithm, group=group)
