@@ -457,7 +457,12 @@ def kernel_test(args):
                      "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": None, "alg_bytes_per_launch": alg_bytes,
-                     "kernel_ms": round(call_s * 1e3, 4)},
+                     "kernel_ms": round(call_s * 1e3, 4),
+                     "median_call_ms": round(float(np.median(call_ms)), 4)},
+        "snapshot": ("no copy of the matrices: every minibatch reads the unchanged "
+                     "matrices and its updates go to " +
+                     ("staging rows summed in a fixed order" if srt else
+                      "fp64 delta buffers") + ", applied after all minibatches"),
     }
     if not args.no_cpu_baseline:
         import oracle
