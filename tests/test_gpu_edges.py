@@ -159,3 +159,18 @@ def test_dropped_minibatch_is_reported_to_a_caller_without_stats():
     w2v.train_epoch(good, gi, go, tb, None, window=3, K=2)
     w2v.device_status()
 
+
+
+def test_default_concurrency_caps():
+    """Reading R24: the default launch is the wavefronts the GPU holds, capped
+    by the vocabulary (V / (4 G (2 window + K + 1))) and by K (131072 /
+    (K + 1), the bound under which the 10^6-word epoch stayed finite at
+    K = 64)."""
+    held = w2v.default_inflight(300, 5, 5, V=10**9)   # no vocabulary or K cap binds
+    assert held >= 2048
+    assert w2v.default_inflight(300, 5, 5, V=10**6) == held
+    # K = 64: 131072 / 65 = 2016, below what the GPU holds for either D
+    assert w2v.default_inflight(100, 5, 64, V=10**6) == 131072 // 65
+    assert w2v.default_inflight(300, 5, 64, V=10**6) == 131072 // 65
+    assert w2v.default_inflight(64, 5, 5, V=1000) == 1000 // (4 * 16)
+    assert w2v.default_inflight(64, 5, 5, V=1000, group=4) == max(1, 1000 // (4 * 4 * 16))
