@@ -224,18 +224,29 @@ __global__ __launch_bounds__(kTotalsThreads) void k_vocab_plan(const int64_t* pa
 // would otherwise serialise the atomic on one address). The counters go to
 // partial[u][0..kBinIds). Grid: an upper bound on the number of units; the
 // workgroups past the plan's count return at once.
+// Start chunks: wstart[k] = the chunk whose run holds int4 k * kWindow4 of
+// the batch, so the chunk of int4 v lies in [wstart[v / kWindow4],
+// wstart[v / kWindow4 + 1]] (a few chunks) instead of anywhere in the batch.
+constexpr int kWindowShift = 10;
+constexpr int32_t kWindow4 = 1 << kWindowShift;
+constexpr int kMaxWindows = (int)(kTallyBatch * (kChunkStride / 4) / kWindow4) + 2;
+
 struct TallyRun {
   const int32_t* binned;
   const int32_t* pre;
   const int32_t* sbeg;
+  const int32_t* wstart;
   int64_t cb;
   int nb;
   int32_t total4;
+  int32_t nwin;
 };
 
 __device__ __forceinline__ int4 tally_load(const TallyRun& r, int32_t v) {
   if (v >= r.total4) return make_int4(-1, -1, -1, -1);
-  int l = 0, h = r.nb - 1;  // last chunk with pre[l] <= v
+  const int w = v >> kWindowShift;
+  int l = r.wstart[w];       // last chunk with pre[l] <= v
+  int h = w + 1 < r.nwin ? r.wstart[w + 1] : r.nb - 1;
   while (l < h) {
     const int m = (l + h + 1) / 2;
     if (r.pre[m] <= v) l = m; else h = m - 1;
@@ -260,6 +271,7 @@ __global__ __launch_bounds__(kTallyThreads) void k_vocab_tally(
   __shared__ int32_t pre[kTallyBatch + 1];
   __shared__ int32_t sbeg[kTallyBatch];
   __shared__ int32_t wsum[kTallyThreads / kWave];
+  __shared__ int32_t wstart[kMaxWindows];
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
   const int wave = tid / kWave;
@@ -303,6 +315,13 @@ __global__ __launch_bounds__(kTallyThreads) void k_vocab_tally(
       sbeg[tid] = s;
     }
     if (tid == 0) pre[0] = 0;
+    // the start chunk of every window of kWindow4 int4 that begins in this
+    // thread's run (an empty run starts none)
+    if (tid < nb) {
+      const int32_t a = incl - len4;
+      for (int32_t w = (a + kWindow4 - 1) >> kWindowShift; w * kWindow4 < incl; ++w)
+        wstart[w] = tid;
+    }
     __syncthreads();
     // the next batch's bounds, in flight while this batch is counted
     s = 0;
@@ -312,7 +331,9 @@ __global__ __launch_bounds__(kTallyThreads) void k_vocab_tally(
       s = row[b];
       e = row[b + 1];
     }
-    const TallyRun run{binned, pre, sbeg, cb, nb, pre[nb]};
+    const int32_t total4 = pre[nb];
+    const TallyRun run{binned, pre,    sbeg, wstart, cb,
+                       nb,     total4, (total4 + kWindow4 - 1) >> kWindowShift};
     constexpr int32_t kStep = kTallyThreads * kTallyUnroll;
     int4 q[kTallyUnroll];
 #pragma unroll
