@@ -215,7 +215,8 @@ __global__ __launch_bounds__(kTotalsThreads) void k_vocab_plan(const int64_t* pa
 // (c) Unit u = (bin b, chunks [c0, c1)): kBinIds LDS counters; the
 // segments of up to kTallyBatch chunks at a time are read as one run of
 // int4 (a block-wide scan of their lengths; each thread finds the chunk of
-// an int4 by binary search over the scan). Loads are software-pipelined:
+// an int4 by binary search over the scan, between the start chunks of the
+// two kWindow4-int4 windows around it). Loads are software-pipelined:
 // each thread has kTallyUnroll int4 in flight while it adds the previous
 // kTallyUnroll, and the next batch's segment bounds are loaded while the
 // current batch is counted. One LDS atomic per id, except that the id of the
